@@ -1,0 +1,158 @@
+/*
+ * losa.h -- C ABI of liblosa.so, the MI355X (gfx950) hot path of LoSA
+ * ("Near-Lossless Sparse Attention for Training-Free Video Diffusion
+ * Acceleration"): exact block masses at the construction step, the
+ * shortest-prefix block selection, and block-sparse attention over the frozen
+ * support.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All tensor pointers are caller-owned HIP DEVICE memory (16-byte aligned)
+ *   unless stated otherwise.  The library never allocates device memory and
+ *   keeps no state between calls except a thread-local error string.
+ * - Q, K, V, O are contiguous [B][H][N_pad][d] in the element type `dtype`,
+ *   N_pad = N rounded up to max(block_q, block_k).  Token positions n >= N
+ *   are padding: as keys they never enter a softmax; as queries they are left
+ *   out of every block mass and their output rows are written as 0 (lse as
+ *   -inf).  Padding rows of Q/K/V may hold any finite values.
+ * - n_q = N_pad / block_q query blocks and n_k = N_pad / block_k key/value
+ *   blocks per head (the partition of Sec. 3.1); row r = (b*H + h)*n_q + i
+ *   addresses query block i of head h in batch b (a classifier-free-guidance
+ *   branch is simply another b).
+ * - `scale` multiplies Q K^T before the softmax; the method uses 1/sqrt(d).
+ * - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *   asynchronously; outputs are valid once the stream has reached that point.
+ * - Validation is synchronous and happens before any HIP call: on an error
+ *   nothing is launched, outputs are untouched, and losa_last_error() holds a
+ *   description.  Launch failures return LOSA_ERR_HIP.
+ * - Supported (v1): dtype BF16 or F32, d in {64, 128}, block_q == block_k in
+ *   {64, 128}.  Other valid combinations return LOSA_ERR_UNSUPPORTED.
+ * - Calls are deterministic: the same inputs give bitwise identical outputs.
+ */
+#ifndef LOSA_H
+#define LOSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LOSA_OK = 0,
+  LOSA_ERR_NULL_POINTER = 1,  /* a required pointer is NULL                              */
+  LOSA_ERR_INVALID_SHAPE = 2, /* B, H, N, d <= 0; block not a power of two in [16, 256];
+                                 sizes overflow the 32-bit index ranges of the kernels    */
+  LOSA_ERR_INVALID_TAU = 3,   /* tau is NaN or not in (0, 1]                              */
+  LOSA_ERR_ALIGNMENT = 4,     /* a tensor pointer is not 16-byte aligned                  */
+  LOSA_ERR_UNSUPPORTED = 5,   /* valid, but not implemented (see "Supported" above)       */
+  LOSA_ERR_CAPACITY = 6,      /* col_idx capacity or workspace too small                  */
+  LOSA_ERR_HIP = 7            /* a HIP runtime / launch error; see losa_last_error()      */
+} losa_status;
+
+typedef enum { LOSA_DTYPE_F32 = 0, LOSA_DTYPE_BF16 = 1 } losa_dtype;
+
+/*
+ * Exact block attention masses of one dense step (Sec. 3.1, Eq. (1); used at
+ * the construction step t0 of Sec. 4.1).
+ *
+ * For every (b, h, i) with R_i >= 1 valid query rows:
+ *   mass[b][h][i][j] = (1/R_i) * sum_{q in B^Q_i, q < N} sum_{k in B^K_j, k < N} A(q, k),
+ *   A(q, .) = softmax over the N valid keys of scale * Q[q] . K[k],
+ * i.e. Eq. (1)'s M(i, j) divided by R_i, so each row of `mass` sums to 1 (the
+ * paper's threshold theta*R then reads mass >= theta).  Rows of query blocks
+ * with no valid query are all zero; key blocks with no valid key get 0.
+ *
+ * q, k       [B][H][N_pad][d] of `dtype` (read only).
+ * mass       out, fp32 [B][H][n_q][n_k].
+ * lse        out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp of the
+ *            scaled scores of each query over all valid keys; -inf on padding.
+ * workspace  unused in v1 (may be NULL; losa_workspace_bytes(0, ...) = 0).
+ * Arithmetic: bf16 inputs use bf16 matrix-core products with fp32
+ * accumulation; f32 inputs use fp32 throughout.
+ */
+losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, int B, int H,
+                                int N, int d, int block_q, int block_k, float scale, float* mass,
+                                float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/*
+ * Shortest-prefix selection of retained key blocks and its CSR storage
+ * (Sec. 4.1, Eq. (3)).
+ *
+ * For each row r: order the row's key blocks by decreasing mass, ties by the
+ * smaller block index (the paper leaves ties arbitrary); keep the shortest
+ * prefix whose cumulative mass (summed in fp64) reaches tau (the exact fp32
+ * value passed).  tau >= 1 keeps every key block that holds a valid key, so
+ * the sparse forward then equals dense attention.  A row whose masses never
+ * reach tau also keeps every such block.  Rows of query blocks with no valid
+ * query are empty.  Masses that are negative or NaN count as 0.
+ *
+ * mass              fp32 [B][H][n_q][n_k] (e.g. from losa_calibrate_mass).
+ * row_ptr           out, int32 [B*H*n_q + 1]: row_ptr[0] = 0, row_ptr[end] = nnz.
+ * col_idx           out, int32: row r's kept block ids, strictly ascending, at
+ *                   col_idx[row_ptr[r] .. row_ptr[r+1]).
+ * col_idx_capacity  elements available at col_idx; must be >= B*H*n_q*n_k
+ *                   (the worst case), checked before launching.
+ * workspace         >= losa_workspace_bytes(1, ...) bytes of device memory.
+ * nnz is produced on the device (row_ptr[B*H*n_q]); read it after a sync.
+ */
+losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block_q, int block_k,
+                               float tau, int32_t* row_ptr, int32_t* col_idx,
+                               int64_t col_idx_capacity, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/*
+ * Frozen-support block-sparse attention (Sec. 4.2, Eq. (4)).
+ *
+ * For every valid query q of query block i in head (b, h):
+ *   O[q] = sum_{k in K(q)} softmax_{K(q)}(scale * Q[q] . K[k]) V[k],
+ *   K(q) = union over j in col_idx[row_ptr[r] .. row_ptr[r+1]) of the valid
+ *          keys of key block j,
+ * i.e. the softmax is renormalised over the retained keys only.  Reused
+ * unchanged across the later steps (Sec. 4.2): only Q, K, V change.
+ *
+ * q, k, v     [B][H][N_pad][d] of `dtype`.
+ * row_ptr     int32 [B*H*n_q + 1]; col_idx int32 [col_idx_len].  A row's ids
+ *             must be distinct (any order); ids outside [0, n_k) are ignored;
+ *             row bounds are clamped to [0, col_idx_len], so a malformed CSR
+ *             cannot make the kernel read outside col_idx.
+ * o           out, [B][H][N_pad][d] of `dtype`.  Rows with an empty key set and
+ *             padding rows are 0.
+ * lse         out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp over
+ *             K(q) of the scaled scores; -inf for empty or padding rows.
+ * workspace   >= losa_workspace_bytes(2, ...) bytes (bf16: a transposed copy
+ *             of V, B*H*N_pad*d*2 bytes; f32: none).
+ * Arithmetic (bf16): Q K^T and P V on bf16 matrix cores with fp32
+ * accumulation, softmax in fp32, P rounded to bf16 for the P V product, O
+ * rounded to bf16 once at the end.  f32: fp32 throughout.
+ */
+losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
+                                 int B, int H, int N, int d, int block_q, int block_k,
+                                 float scale, const int32_t* row_ptr, const int32_t* col_idx,
+                                 int64_t col_idx_len, void* o, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace bytes needed by: which = 0 losa_calibrate_mass, 1 losa_select_blocks,
+ * 2 losa_sparse_attn_fwd.  Returns 0 for invalid arguments (then the call
+ * itself reports the error).
+ */
+size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
+                            int block_k);
+
+/* Static text for a status code ("LOSA_OK", ...). */
+const char* losa_status_string(losa_status s);
+
+/* Thread-local description of the last non-OK status returned on this thread. */
+const char* losa_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int losa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOSA_H */

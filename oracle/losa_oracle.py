@@ -111,7 +111,7 @@ def dense_probabilities(q, k, N: int, scale: float, b: int = 0, h: int = 0):
 # block attention mass (Sec. 3.1, Eq. (1))
 # ----------------------------------------------------------------------------
 
-def block_masses(q, k, N: int, block_q: int, block_k: int, scale: float):
+def block_masses(q, k, N: int, block_q: int, block_k: int, scale: float, rows_subset=None):
     """Exact block masses of the dense step.
 
     For each (b, h, i): A = softmax over all N valid keys of scale * q k^T for
@@ -120,6 +120,8 @@ def block_masses(q, k, N: int, block_q: int, block_k: int, scale: float):
 
     Returns (mbar [B,H,n_q,n_k] fp64, lse [B,H,N_pad] fp64, natural log; -inf
     on padding rows).  A query block with no valid row gets an all-zero row.
+    ``rows_subset``: optional iterable of rows r = (b*H + h)*n_q + i to compute
+    (the others stay zero / -inf).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -127,22 +129,22 @@ def block_masses(q, k, N: int, block_q: int, block_k: int, scale: float):
     n_q, n_k = Np // block_q, Np // block_k
     mbar = np.zeros((B, H, n_q, n_k))
     lse = np.full((B, H, Np), -np.inf)
-    for b in range(B):
-        for h in range(H):
-            kv = k[b, h, :N]
-            for i in range(n_q):
-                rows = valid_rows(i, block_q, N)
-                if rows.size == 0:
-                    continue
-                S = scale * (q[b, h, rows] @ kv.T)
-                A, l = row_softmax(S)
-                lse[b, h, rows] = l
-                # per-row mass of every key block: sum the probabilities of its
-                # valid keys (padding keys carry no probability)
-                Apad = np.zeros((rows.size, n_k * block_k))
-                Apad[:, :N] = A
-                Mrow = Apad.reshape(rows.size, n_k, block_k).sum(axis=2)
-                mbar[b, h, i] = Mrow.mean(axis=0)
+    todo = range(B * H * n_q) if rows_subset is None else rows_subset
+    for r in todo:
+        b, rem = divmod(int(r), H * n_q)
+        h, i = divmod(rem, n_q)
+        rows = valid_rows(i, block_q, N)
+        if rows.size == 0:
+            continue
+        S = scale * (q[b, h, rows] @ k[b, h, :N].T)
+        A, l = row_softmax(S)
+        lse[b, h, rows] = l
+        # per-row mass of every key block: sum the probabilities of its valid
+        # keys (padding keys carry no probability)
+        Apad = np.zeros((rows.size, n_k * block_k))
+        Apad[:, :N] = A
+        Mrow = Apad.reshape(rows.size, n_k, block_k).sum(axis=2)
+        mbar[b, h, i] = Mrow.mean(axis=0)
     return mbar, lse
 
 
@@ -177,9 +179,14 @@ def select_row(mrow, tau: float, n_k_valid: int, has_valid_rows: bool = True) ->
         omega = np.arange(n_k_valid)
     else:
         hit = np.nonzero(cum >= tau)[0]
-        s = int(hit[0]) + 1 if hit.size else n_k_valid
-        s = max(s, 1)
-        omega = np.sort(order[:s])
+        if hit.size:
+            s = max(int(hit[0]) + 1, 1)
+            omega = np.sort(order[:s])
+        else:
+            # the masses never reach tau (they sum below it): keep every
+            # block that holds a valid key, as for tau >= 1
+            s = n_k_valid
+            omega = np.arange(n_k_valid)
     return RowSelection(order=order, cum=cum, s=s, omega=omega.astype(np.int64))
 
 

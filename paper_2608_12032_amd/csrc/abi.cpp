@@ -1,0 +1,219 @@
+// C ABI of liblosa.so: argument validation, workspace sizing, dispatch to the
+// HIP launchers, and status reporting.  See include/losa.h for the contract.
+#include "losa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+losa_status fail(losa_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+bool pow2_in(int x, int lo, int hi) { return x >= lo && x <= hi && (x & (x - 1)) == 0; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Shape {
+  int B, H, N, d, bq, bk;
+  int n_pad, n_q, n_k;
+  int64_t rows;
+};
+
+// Checks shared by every entry point.  Fills `s` on success.
+losa_status check_shape(int B, int H, int N, int d, int bq, int bk, Shape* s) {
+  if (B <= 0 || H <= 0 || N <= 0 || d <= 0)
+    return fail(LOSA_ERR_INVALID_SHAPE, "B=%d H=%d N=%d d=%d must all be > 0", B, H, N, d);
+  if (!pow2_in(bq, 16, 256) || !pow2_in(bk, 16, 256))
+    return fail(LOSA_ERR_INVALID_SHAPE, "block_q=%d block_k=%d must be powers of two in [16,256]",
+                bq, bk);
+  const int64_t L = bq > bk ? bq : bk;
+  const int64_t n_pad = (N + L - 1) / L * L;
+  // kernels index one head with 32-bit byte offsets (fp32 elements at most)
+  if (n_pad * (int64_t)d * 4 >= ((int64_t)1 << 31))
+    return fail(LOSA_ERR_INVALID_SHAPE, "N_pad*d = %lld exceeds the per-head index range",
+                (long long)(n_pad * d));
+  const int64_t rows = (int64_t)B * H * (n_pad / bq);
+  if (rows >= ((int64_t)1 << 31) || (int64_t)B * H >= 65536)
+    return fail(LOSA_ERR_INVALID_SHAPE, "B*H*n_q = %lld rows is too many", (long long)rows);
+  s->B = B;
+  s->H = H;
+  s->N = N;
+  s->d = d;
+  s->bq = bq;
+  s->bk = bk;
+  s->n_pad = (int)n_pad;
+  s->n_q = (int)(n_pad / bq);
+  s->n_k = (int)(n_pad / bk);
+  s->rows = rows;
+  return LOSA_OK;
+}
+
+losa_status check_supported(losa_dtype dtype, const Shape& s) {
+  if (dtype != LOSA_DTYPE_F32 && dtype != LOSA_DTYPE_BF16)
+    return fail(LOSA_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+  if (s.d != 64 && s.d != 128)
+    return fail(LOSA_ERR_UNSUPPORTED, "head dim d=%d not supported (64 or 128)", s.d);
+  if (s.bq != s.bk)
+    return fail(LOSA_ERR_UNSUPPORTED, "block_q=%d != block_k=%d not supported", s.bq, s.bk);
+  if (s.bq != 64 && s.bq != 128)
+    return fail(LOSA_ERR_UNSUPPORTED, "block %d not supported (64 or 128)", s.bq);
+  return LOSA_OK;
+}
+
+losa_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return LOSA_OK;
+  return fail(LOSA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t elem_bytes(losa_dtype dt) { return dt == LOSA_DTYPE_BF16 ? 2 : 4; }
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+}  // namespace
+
+extern "C" {
+
+losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, int B, int H,
+                                int N, int d, int block_q, int block_k, float scale, float* mass,
+                                float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!q || !k || !mass) return fail(LOSA_ERR_NULL_POINTER, "q, k and mass must be non-NULL");
+  Shape s;
+  losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
+  if (st != LOSA_OK) return st;
+  if (!std::isfinite(scale)) return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(mass) || (lse && !aligned16(lse)))
+    return fail(LOSA_ERR_ALIGNMENT, "tensor pointers must be 16-byte aligned");
+  st = check_supported(dtype, s);
+  if (st != LOSA_OK) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (dtype == LOSA_DTYPE_BF16) {
+    if (losa::calib_bf16_lds_bytes(d, block_q, s.n_k) > kMaxLds)
+      return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks exceed the calibration LDS budget",
+                  s.n_k);
+    return hip_status(
+        losa::launch_calibrate_bf16(d, block_q, q, k, B, H, N, s.n_pad, scale, mass, lse, hs),
+        "losa_calibrate_mass");
+  }
+  return hip_status(
+      losa::launch_calibrate_f32(d, block_q, q, k, B, H, N, s.n_pad, scale, mass, lse, hs),
+      "losa_calibrate_mass");
+}
+
+losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block_q, int block_k,
+                               float tau, int32_t* row_ptr, int32_t* col_idx,
+                               int64_t col_idx_capacity, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  if (!mass || !row_ptr || !col_idx || !workspace)
+    return fail(LOSA_ERR_NULL_POINTER, "mass, row_ptr, col_idx and workspace must be non-NULL");
+  Shape s;
+  losa_status st = check_shape(B, H, N, 1, block_q, block_k, &s);
+  if (st != LOSA_OK) return st;
+  if (std::isnan(tau) || !(tau > 0.f) || tau > 1.f)
+    return fail(LOSA_ERR_INVALID_TAU, "tau=%g must be in (0, 1]", (double)tau);
+  if (!aligned16(mass) || !aligned16(row_ptr) || !aligned16(col_idx) || !aligned16(workspace))
+    return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
+  if (s.n_k > losa::select_max_nk())
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per row exceeds %d", s.n_k,
+                losa::select_max_nk());
+  const int64_t worst = s.rows * s.n_k;
+  if (worst >= ((int64_t)1 << 31))
+    return fail(LOSA_ERR_INVALID_SHAPE, "rows*n_k=%lld exceeds the int32 CSR range",
+                (long long)worst);
+  if (col_idx_capacity < worst)
+    return fail(LOSA_ERR_CAPACITY, "col_idx_capacity=%lld < B*H*n_q*n_k=%lld",
+                (long long)col_idx_capacity, (long long)worst);
+  const size_t need = losa::select_workspace_bytes((int)s.rows, s.n_k);
+  if (workspace_bytes < need)
+    return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
+  return hip_status(losa::launch_select(mass, B, H, N, block_q, block_k, tau, row_ptr, col_idx,
+                                        workspace, static_cast<hipStream_t>(stream)),
+                    "losa_select_blocks");
+}
+
+losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
+                                 int B, int H, int N, int d, int block_q, int block_k,
+                                 float scale, const int32_t* row_ptr, const int32_t* col_idx,
+                                 int64_t col_idx_len, void* o, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  if (!q || !k || !v || !row_ptr || !o)
+    return fail(LOSA_ERR_NULL_POINTER, "q, k, v, row_ptr and o must be non-NULL");
+  if (col_idx_len < 0) return fail(LOSA_ERR_INVALID_SHAPE, "col_idx_len must be >= 0");
+  if (col_idx_len > 0 && !col_idx)
+    return fail(LOSA_ERR_NULL_POINTER, "col_idx is NULL but col_idx_len > 0");
+  Shape s;
+  losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
+  if (st != LOSA_OK) return st;
+  if (!std::isfinite(scale)) return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+      (lse && !aligned16(lse)) || !aligned16(row_ptr) || (col_idx && !aligned16(col_idx)))
+    return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
+  st = check_supported(dtype, s);
+  if (st != LOSA_OK) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (dtype == LOSA_DTYPE_BF16) {
+    const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d);
+    if (!workspace) return fail(LOSA_ERR_NULL_POINTER, "bf16 needs a workspace of %zu bytes", need);
+    if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
+    if (workspace_bytes < need)
+      return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
+    return hip_status(losa::launch_sparse_fwd_bf16(d, block_q, q, k, v, B, H, N, s.n_pad, scale,
+                                                   row_ptr, col_idx, col_idx_len, o, lse,
+                                                   workspace, hs),
+                      "losa_sparse_attn_fwd");
+  }
+  return hip_status(losa::launch_sparse_fwd_f32(d, block_q, q, k, v, B, H, N, s.n_pad, scale,
+                                                row_ptr, col_idx, col_idx_len, o, lse, hs),
+                    "losa_sparse_attn_fwd");
+}
+
+size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
+                            int block_k) {
+  Shape s;
+  if (check_shape(B, H, N, which == 1 ? 1 : d, block_q, block_k, &s) != LOSA_OK) return 0;
+  switch (which) {
+    case 0:
+      return 0;
+    case 1:
+      return losa::select_workspace_bytes((int)s.rows, s.n_k);
+    case 2:
+      return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d) : 0;
+    default:
+      return 0;
+  }
+}
+
+const char* losa_status_string(losa_status s) {
+  switch (s) {
+    case LOSA_OK: return "LOSA_OK";
+    case LOSA_ERR_NULL_POINTER: return "LOSA_ERR_NULL_POINTER";
+    case LOSA_ERR_INVALID_SHAPE: return "LOSA_ERR_INVALID_SHAPE";
+    case LOSA_ERR_INVALID_TAU: return "LOSA_ERR_INVALID_TAU";
+    case LOSA_ERR_ALIGNMENT: return "LOSA_ERR_ALIGNMENT";
+    case LOSA_ERR_UNSUPPORTED: return "LOSA_ERR_UNSUPPORTED";
+    case LOSA_ERR_CAPACITY: return "LOSA_ERR_CAPACITY";
+    case LOSA_ERR_HIP: return "LOSA_ERR_HIP";
+  }
+  return "LOSA_ERR_UNKNOWN";
+}
+
+const char* losa_last_error(void) { return g_err; }
+
+int losa_version(void) { return 100; }
+
+}  // extern "C"

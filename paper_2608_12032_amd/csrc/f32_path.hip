@@ -1,0 +1,237 @@
+// fp32 inputs: block masses (Sec. 3.1, Eq. (1)) and frozen-support attention
+// (Sec. 4.2, Eq. (4)) with fp32 vector arithmetic throughout.
+//
+// fp32 is the small-workload path (no bf16 rounding anywhere), so these
+// kernels keep to a plain layout: one thread per query row, one workgroup per
+// query block, key/value rows staged through LDS in chunks of 32 keys and read
+// by every thread as broadcasts.  Masking and padding follow the bf16 kernels:
+// keys >= N never enter a softmax, query rows >= N get O = 0 and lse = -inf,
+// and so do rows whose key set is empty; col_idx entries outside [0, n_k) are
+// ignored and row bounds are clamped to [0, col_idx_len].
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace losa {
+
+namespace {
+
+constexpr int CK = 32;  // keys per LDS chunk
+
+template <int D, int BLK>
+__device__ __forceinline__ void stage_rows(float* dst, const float* src, int key0, int t) {
+  // CK consecutive rows of D floats starting at row key0 of src
+  for (int idx = t; idx < CK * D / 4; idx += BLK) {
+    const int row = idx / (D / 4);
+    const int col = (idx % (D / 4)) * 4;
+    *reinterpret_cast<f32x4_t*>(dst + row * D + col) =
+        *reinterpret_cast<const f32x4_t*>(src + (size_t)(key0 + row) * D + col);
+  }
+}
+
+template <int D, int BLK>
+__global__ void __launch_bounds__(BLK)
+    sparse_fwd_f32_kernel(const float* __restrict__ Q, const float* __restrict__ K,
+                          const float* __restrict__ V, const int32_t* __restrict__ row_ptr,
+                          const int32_t* __restrict__ col_idx, int64_t col_len,
+                          float* __restrict__ O, float* __restrict__ lse, int n_q, int n_k, int N,
+                          int n_pad, float scale_log2) {
+  __shared__ __attribute__((aligned(16))) float Kc[CK * D];
+  __shared__ __attribute__((aligned(16))) float Vc[CK * D];
+  const int t = threadIdx.x;
+  const int r = blockIdx.x;
+  const int bh = r / n_q;
+  const int i = r - bh * n_q;
+  const size_t head = (size_t)bh * n_pad * D;
+  const int qrow = i * BLK + t;
+
+  float q[D], o[D];
+#pragma unroll
+  for (int dd = 0; dd < D; ++dd) {
+    q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
+    o[dd] = 0.f;
+  }
+  float m = kNegBig, l = 0.f;
+
+  int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
+  e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
+  e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
+  for (int64_t e = e0; e < e1; ++e) {
+    const int j = col_idx[e];
+    if (j < 0 || j >= n_k) continue;
+    const int kvalid = min(BLK, N - j * BLK);
+    for (int c0 = 0; c0 < kvalid; c0 += CK) {
+      __syncthreads();
+      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
+      stage_rows<D, BLK>(Vc, V + head, j * BLK + c0, t);
+      __syncthreads();
+      const int nk = min(CK, kvalid - c0);
+      float s[CK];
+      float mx = m;
+#pragma unroll
+      for (int kk = 0; kk < CK; ++kk) {
+        float acc = 0.f;
+#pragma unroll
+        for (int dd = 0; dd < D; ++dd) acc = fmaf(q[dd], Kc[kk * D + dd], acc);
+        s[kk] = kk < nk ? acc : -INFINITY;
+        mx = fmaxf(mx, s[kk]);
+      }
+      const float alpha = fast_exp2(m - mx);
+      m = mx;
+      l *= alpha;
+#pragma unroll
+      for (int dd = 0; dd < D; ++dd) o[dd] *= alpha;
+#pragma unroll
+      for (int kk = 0; kk < CK; ++kk) {
+        const float p = fast_exp2(s[kk] - m);
+        l += p;
+#pragma unroll
+        for (int dd = 0; dd < D; ++dd) o[dd] = fmaf(p, Vc[kk * D + dd], o[dd]);
+      }
+    }
+  }
+  const bool ok = (qrow < N) && (l > 0.f);
+  const float inv = ok ? 1.0f / l : 0.f;
+#pragma unroll
+  for (int dd = 0; dd < D; ++dd) O[head + (size_t)qrow * D + dd] = o[dd] * inv;
+  if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = ok ? (m + __log2f(l)) * kLn2 : -INFINITY;
+}
+
+template <int D, int BLK>
+__global__ void __launch_bounds__(BLK)
+    calib_f32_kernel(const float* __restrict__ Q, const float* __restrict__ K,
+                     float* __restrict__ mass, float* __restrict__ lse, int n_q, int n_k, int N,
+                     int n_pad, float scale_log2) {
+  constexpr int NW = BLK / 64;
+  __shared__ __attribute__((aligned(16))) float Kc[CK * D];
+  __shared__ float red[NW];
+  const int t = threadIdx.x;
+  const int r = blockIdx.x;
+  const int bh = r / n_q;
+  const int i = r - bh * n_q;
+  const size_t head = (size_t)bh * n_pad * D;
+  const int qrow = i * BLK + t;
+  const int rows_valid = min(BLK, N - i * BLK);
+  float* mrow = mass + (size_t)r * n_k;
+  if (rows_valid <= 0) {
+    for (int j = t; j < n_k; j += BLK) mrow[j] = 0.f;
+    if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = -INFINITY;
+    return;
+  }
+  float q[D];
+#pragma unroll
+  for (int dd = 0; dd < D; ++dd) q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
+  const int n_kv = (N + BLK - 1) / BLK;
+
+  // sweep 1: running max / sum over every valid key
+  float m = kNegBig, l = 0.f;
+  for (int j = 0; j < n_kv; ++j) {
+    const int kvalid = min(BLK, N - j * BLK);
+    for (int c0 = 0; c0 < kvalid; c0 += CK) {
+      __syncthreads();
+      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
+      __syncthreads();
+      const int nk = min(CK, kvalid - c0);
+      float s[CK];
+      float mx = m;
+#pragma unroll
+      for (int kk = 0; kk < CK; ++kk) {
+        float acc = 0.f;
+#pragma unroll
+        for (int dd = 0; dd < D; ++dd) acc = fmaf(q[dd], Kc[kk * D + dd], acc);
+        s[kk] = kk < nk ? acc : -INFINITY;
+        mx = fmaxf(mx, s[kk]);
+      }
+      l *= fast_exp2(m - mx);
+      m = mx;
+#pragma unroll
+      for (int kk = 0; kk < CK; ++kk) l += fast_exp2(s[kk] - m);
+    }
+  }
+  const bool qvalid = qrow < N;
+  const float lse2 = m + __log2f(l);
+  if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = qvalid ? lse2 * kLn2 : -INFINITY;
+  const float sub = qvalid ? lse2 : INFINITY;
+
+  // sweep 2: per key block, sum of normalised probabilities over the rows
+  const int lane = t & 63, w = t >> 6;
+  const float inv_rows = 1.0f / (float)rows_valid;
+  for (int j = 0; j < n_kv; ++j) {
+    const int kvalid = min(BLK, N - j * BLK);
+    float acc = 0.f;
+    for (int c0 = 0; c0 < kvalid; c0 += CK) {
+      __syncthreads();
+      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
+      __syncthreads();
+      const int nk = min(CK, kvalid - c0);
+#pragma unroll
+      for (int kk = 0; kk < CK; ++kk) {
+        float s = 0.f;
+#pragma unroll
+        for (int dd = 0; dd < D; ++dd) s = fmaf(q[dd], Kc[kk * D + dd], s);
+        acc += kk < nk ? fast_exp2(s - sub) : 0.f;
+      }
+    }
+    acc = wave_sum(acc);
+    __syncthreads();
+    if (lane == 0) red[w] = acc;
+    __syncthreads();
+    if (t == 0) {
+      float tot = 0.f;
+      for (int ww = 0; ww < NW; ++ww) tot += red[ww];
+      mrow[j] = tot * inv_rows;
+    }
+  }
+  for (int j = n_kv + t; j < n_k; j += BLK) mrow[j] = 0.f;
+}
+
+template <int D, int BLK>
+hipError_t launch_f32(const void* q, const void* k, const void* v, int B, int H, int N, int n_pad,
+                      float scale, const int32_t* row_ptr, const int32_t* col_idx,
+                      int64_t col_len, void* o, float* lse, hipStream_t stream) {
+  const int n_q = n_pad / BLK, n_k = n_pad / BLK;
+  hipLaunchKernelGGL((sparse_fwd_f32_kernel<D, BLK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
+                     static_cast<const float*>(q), static_cast<const float*>(k),
+                     static_cast<const float*>(v), row_ptr, col_idx, col_len,
+                     static_cast<float*>(o), lse, n_q, n_k, N, n_pad, scale * kLog2e);
+  return hipGetLastError();
+}
+
+template <int D, int BLK>
+hipError_t launch_cal_f32(const void* q, const void* k, int B, int H, int N, int n_pad, float scale,
+                          float* mass, float* lse, hipStream_t stream) {
+  const int n_q = n_pad / BLK, n_k = n_pad / BLK;
+  hipLaunchKernelGGL((calib_f32_kernel<D, BLK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
+                     static_cast<const float*>(q), static_cast<const float*>(k), mass, lse, n_q,
+                     n_k, N, n_pad, scale * kLog2e);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sparse_fwd_f32(int d, int blk, const void* q, const void* k, const void* v,
+                                 int B, int H, int N, int n_pad, float scale,
+                                 const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
+                                 void* o, float* lse, hipStream_t stream) {
+#define LOSA_F32_FWD(DD, BB)                                                                 \
+  if (d == DD && blk == BB)                                                                  \
+    return launch_f32<DD, BB>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, \
+                              lse, stream);
+  LOSA_F32_FWD(64, 64)
+  LOSA_F32_FWD(64, 128)
+  LOSA_F32_FWD(128, 64)
+  LOSA_F32_FWD(128, 128)
+#undef LOSA_F32_FWD
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_calibrate_f32(int d, int blk, const void* q, const void* k, int B, int H, int N,
+                                int n_pad, float scale, float* mass, float* lse,
+                                hipStream_t stream) {
+  if (d == 64 && blk == 64) return launch_cal_f32<64, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  if (d == 64 && blk == 128) return launch_cal_f32<64, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  if (d == 128 && blk == 64) return launch_cal_f32<128, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  if (d == 128 && blk == 128) return launch_cal_f32<128, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace losa

@@ -1,0 +1,175 @@
+"""Thin Python binding of liblosa.so (include/losa.h).
+
+Argument marshalling only: torch tensors in, device pointers and sizes out,
+the current HIP stream passed through.  Every step of the computation runs in
+the library's HIP kernels; if the library is missing this module raises on
+import instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblosa.so")
+
+LOSA_DTYPE_F32 = 0
+LOSA_DTYPE_BF16 = 1
+STATUS = {0: "LOSA_OK", 1: "LOSA_ERR_NULL_POINTER", 2: "LOSA_ERR_INVALID_SHAPE",
+          3: "LOSA_ERR_INVALID_TAU", 4: "LOSA_ERR_ALIGNMENT", 5: "LOSA_ERR_UNSUPPORTED",
+          6: "LOSA_ERR_CAPACITY", 7: "LOSA_ERR_HIP"}
+
+EXPORTED = ("losa_calibrate_mass", "losa_select_blocks", "losa_sparse_attn_fwd",
+            "losa_workspace_bytes", "losa_status_string", "losa_last_error", "losa_version")
+
+
+class LosaError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2608_12032_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I, F, Z, L = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_int64
+    lib.losa_calibrate_mass.argtypes = [P, P, I, I, I, I, I, I, I, F, P, P, P, Z, P]
+    lib.losa_calibrate_mass.restype = I
+    lib.losa_select_blocks.argtypes = [P, I, I, I, I, I, F, P, P, L, P, Z, P]
+    lib.losa_select_blocks.restype = I
+    lib.losa_sparse_attn_fwd.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, L, P, P, P, Z, P]
+    lib.losa_sparse_attn_fwd.restype = I
+    lib.losa_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
+    lib.losa_workspace_bytes.restype = Z
+    lib.losa_status_string.argtypes = [I]
+    lib.losa_status_string.restype = ctypes.c_char_p
+    lib.losa_last_error.argtypes = []
+    lib.losa_last_error.restype = ctypes.c_char_p
+    lib.losa_version.argtypes = []
+    lib.losa_version.restype = I
+    return lib
+
+
+lib = _load()
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise LosaError(st, where, lib.losa_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return LOSA_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return LOSA_DTYPE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _qkv_shape(q: torch.Tensor):
+    if q.dim() != 4 or not q.is_contiguous() or not q.is_cuda:
+        raise ValueError("expected a contiguous [B, H, N_pad, d] device tensor")
+    return q.shape
+
+
+def padded_len(N: int, block_q: int, block_k: int) -> int:
+    L = max(block_q, block_k)
+    return -(-N // L) * L
+
+
+def workspace_bytes(which: int, dtype_code: int, B, H, N, d, block_q, block_k) -> int:
+    return int(lib.losa_workspace_bytes(which, dtype_code, B, H, N, d, block_q, block_k))
+
+
+def losa_calibrate_mass(q, k, N: int, block_q: int, block_k: int | None = None,
+                        scale: float | None = None, want_lse: bool = True, mass=None, lse=None):
+    """Exact block masses of a dense step -> (mass [B,H,n_q,n_k] fp32, lse or None)."""
+    block_k = block_k or block_q
+    B, H, Np, d = _qkv_shape(q)
+    if k.shape != q.shape or k.dtype != q.dtype:
+        raise ValueError("q and k must have the same shape and dtype")
+    n_q, n_k = Np // block_q, Np // block_k
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if mass is None:
+        mass = torch.empty((B, H, n_q, n_k), dtype=torch.float32, device=q.device)
+    if want_lse and lse is None:
+        lse = torch.empty((B, H, Np), dtype=torch.float32, device=q.device)
+    if not want_lse:
+        lse = None
+    st = lib.losa_calibrate_mass(_ptr(q), _ptr(k), _dtype_code(q), B, H, N, d, block_q, block_k,
+                                 scale, _ptr(mass), _ptr(lse), None, 0, _stream(q.device))
+    _check(st, "losa_calibrate_mass")
+    return mass, lse
+
+
+def losa_select_blocks(mass, N: int, block_q: int, block_k: int | None, tau: float,
+                       row_ptr=None, col_idx=None, workspace=None):
+    """Shortest-prefix selection -> (row_ptr int32 [rows+1], col_idx int32 buffer).
+
+    col_idx has the worst-case capacity B*H*n_q*n_k; its first row_ptr[-1]
+    entries are valid (read row_ptr[-1] after a sync, or use ``nnz``).
+    """
+    block_k = block_k or block_q
+    B, H, n_q, n_k = mass.shape
+    rows = B * H * n_q
+    dev = mass.device
+    if row_ptr is None:
+        row_ptr = torch.empty(rows + 1, dtype=torch.int32, device=dev)
+    if col_idx is None:
+        col_idx = torch.empty(rows * n_k, dtype=torch.int32, device=dev)
+    need = workspace_bytes(1, LOSA_DTYPE_F32, B, H, N, 1, block_q, block_k)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = lib.losa_select_blocks(_ptr(mass), B, H, N, block_q, block_k, float(tau),
+                                _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(workspace),
+                                workspace.numel(), _stream(dev))
+    _check(st, "losa_select_blocks")
+    return row_ptr, col_idx
+
+
+def nnz(row_ptr) -> int:
+    return int(row_ptr[-1].item())
+
+
+def losa_sparse_attn_fwd(q, k, v, N: int, block_q: int, block_k: int | None, row_ptr, col_idx,
+                         scale: float | None = None, want_lse: bool = False, out=None,
+                         lse=None, workspace=None):
+    """Frozen-support block-sparse attention -> o (and lse if requested)."""
+    block_k = block_k or block_q
+    B, H, Np, d = _qkv_shape(q)
+    for t in (k, v):
+        if t.shape != q.shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError("q, k, v must share shape/dtype and be contiguous")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    dcode = _dtype_code(q)
+    o = torch.empty_like(q) if out is None else out
+    if want_lse and lse is None:
+        lse = torch.empty((B, H, Np), dtype=torch.float32, device=q.device)
+    need = workspace_bytes(2, dcode, B, H, N, d, block_q, block_k)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.losa_sparse_attn_fwd(_ptr(q), _ptr(k), _ptr(v), dcode, B, H, N, d, block_q, block_k,
+                                  scale, _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(o),
+                                  _ptr(lse if want_lse else None), _ptr(workspace), ws_bytes,
+                                  _stream(q.device))
+    _check(st, "losa_sparse_attn_fwd")
+    return (o, lse) if want_lse else o
+
+
+# shorter aliases
+calibrate_mass = losa_calibrate_mass
+select_blocks = losa_select_blocks
+sparse_attn_fwd = losa_sparse_attn_fwd

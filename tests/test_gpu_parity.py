@@ -1,0 +1,352 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Tolerances (from the target): block masses max-abs <= 1e-4; attention outputs
+max-abs <= 2e-2 and mean-abs <= 2e-3 over valid rows (bf16); selected sets
+exact except blocks the oracle's cumulative mass puts within 1e-5 of tau
+(oracle.compare).  Internal, tighter checks: lse within 1e-3; fp32 outputs
+within 1e-4.
+
+The oracle always receives the exact values the GPU received (bf16 and fp32
+upcast exactly to fp64), copied back from the device.  Small cases are checked
+element by element on every row; full-size workloads on sampled rows (first,
+middle, ragged last query block of several heads) plus properties that hold at
+any size.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import compare as CMP
+from oracle import losa_oracle as O
+from paper_2608_12032_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+MASS_TOL = 1e-4
+LSE_TOL = 1e-3
+OUT_MAX, OUT_MEAN = 2e-2, 2e-3
+F32_OUT_MAX = 1e-4
+
+
+@pytest.fixture(scope="module")
+def L():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    from paper_2608_12032_amd import losa
+    return losa
+
+
+def say(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+
+
+def f64(x):
+    return x.detach().float().cpu().numpy().astype(np.float64)
+
+
+def tau32(t):
+    return float(np.float32(t))
+
+
+def sub_csr(rp, ci, rows):
+    rp = np.asarray(rp, dtype=np.int64)
+    ci = np.asarray(ci, dtype=np.int64)
+    out_rp = [0]
+    out_ci = []
+    for r in rows:
+        seg = ci[rp[r]:rp[r + 1]]
+        out_ci.append(seg)
+        out_rp.append(out_rp[-1] + seg.size)
+    return np.array(out_rp), (np.concatenate(out_ci) if out_ci else np.zeros(0, np.int64))
+
+
+def out_tol(w):
+    return (F32_OUT_MAX, F32_OUT_MAX) if w.dtype == "f32" else (OUT_MAX, OUT_MEAN)
+
+
+def sample_rows(w, extra=()):
+    n_q = w.n_blocks
+    heads = sorted({0, w.H - 1, w.H // 2})
+    blocks = sorted({0, 1, n_q // 3, n_q // 2, n_q - 2, n_q - 1, *extra})
+    return [(b * w.H + h) * n_q + i for b in range(w.B) for h in heads for i in blocks
+            if 0 <= i < n_q]
+
+
+def run_case(L, w, tau, reuse=0, rows=None, label=""):
+    """calibrate -> select -> sparse fwd (+ reuse steps), all checked against the oracle."""
+    N, C, scale = w.N, w.block, w.scale
+    n_q = w.n_blocks
+    n_kv = O.num_valid_key_blocks(N, C)
+    t32 = tau32(tau)
+    say(f"{label}: generate {w.name} B={w.B} H={w.H} N={N} d={w.d} block={C} {w.dtype} tau={tau}")
+    state = W.make_state(w, device="cuda")
+    q, k, v = W.cast(state, w)
+
+    say(f"{label}: calibrate")
+    mass, lse = L.losa_calibrate_mass(q, k, N, C)
+    say(f"{label}: select")
+    rp, ci = L.losa_select_blocks(mass, N, C, C, tau)
+    say(f"{label}: sparse fwd step 0")
+    o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, C, C, rp, ci, want_lse=True)
+    torch.cuda.synchronize()
+    say(f"{label}: oracle")
+
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    mass_g, lse_g = f64(mass), f64(lse)
+    rp_g = rp.cpu().numpy().astype(np.int64)
+    nnz = int(rp_g[-1])
+    ci_g = ci[:nnz].cpu().numpy().astype(np.int64)
+    R = w.B * w.H * n_q
+    assert O.validate_csr(rp_g, ci_g, R, n_q, N, C, n_q) == []
+
+    # properties at any size: every row of masses sums to one; recall >= tau
+    sums = mass_g.reshape(R, n_q).sum(axis=1)
+    assert np.all(np.abs(sums - 1.0) < 1e-4), f"mass rows sum to {sums.min()}..{sums.max()}"
+    if t32 < 1:
+        assert O.recall(mass_g, rp_g, ci_g, N, C) >= t32 - 1e-5
+    else:
+        assert nnz == R * n_kv
+
+    todo = list(range(R)) if rows is None else rows
+    m_ref, l_ref = O.block_masses(qh, kh, N, C, C, scale, rows_subset=todo)
+    flat_m_ref = m_ref.reshape(R, n_q)
+    flat_m_g = mass_g.reshape(R, n_q)
+    merr = np.abs(flat_m_g[todo] - flat_m_ref[todo]).max()
+    say(f"{label}: mass max-abs err {merr:.3e}")
+    assert merr <= MASS_TOL
+    qrows = np.concatenate([np.arange(i * C, min((i + 1) * C, N)) + (r // n_q) * w.N_pad
+                            for r in todo for i in [r % n_q]])
+    lerr = np.abs(lse_g.reshape(-1)[qrows] - l_ref.reshape(-1)[qrows]).max()
+    assert lerr <= LSE_TOL, f"lse err {lerr}"
+
+    # selection: the GPU's rows against the oracle's selection on oracle masses
+    details = [O.select_row(flat_m_ref[r], t32, n_kv, (r % n_q) * C < N) for r in todo]
+    srp, sci = sub_csr(rp_g, ci_g, todo)
+    cmp = CMP.compare_selection(srp, sci, details, flat_m_ref[todo], t32)
+    say(f"{label}: selection {cmp}")
+    assert cmp["ok"], cmp
+
+    # sparse forward with the GPU's CSR (isolates Eq. (4) from the selection)
+    tmax, tmean = out_tol(w)
+    for step in range(reuse + 1):
+        if step > 0:
+            W.drift_(state, w, step)
+            q, k, v = W.cast(state, w)
+            say(f"{label}: sparse fwd reuse step {step}")
+            o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, C, C, rp, ci, want_lse=True)
+            torch.cuda.synchronize()
+            qh, kh, vh = f64(q), f64(k), f64(v)
+        o_ref, lo_ref = O.sparse_attention(qh, kh, vh, N, C, C, scale, rp_g, ci_g,
+                                           rows_subset=todo)
+        og = f64(o)
+        err = np.abs(og.reshape(-1, w.d)[qrows] - o_ref.reshape(-1, w.d)[qrows])
+        say(f"{label}: step {step} out max {err.max():.3e} mean {err.mean():.3e}")
+        assert err.max() <= tmax and err.mean() <= tmean
+        lo_err = np.abs(f64(lse_o).reshape(-1)[qrows] - lo_ref.reshape(-1)[qrows]).max()
+        assert lo_err <= LSE_TOL
+        # padding rows are zero, lse -inf
+        og4 = og.reshape(w.B, w.H, w.N_pad, w.d)
+        assert np.all(og4[:, :, N:] == 0)
+        assert np.all(np.isneginf(f64(lse_o)[:, :, N:]))
+    return dict(nnz=nnz, coverage=nnz / (R * n_q), exempt=cmp["exempt"])
+
+
+# ----------------------------------------------------------------------------
+# small cases: every row, several tiles, ragged tails
+# ----------------------------------------------------------------------------
+
+SMALL = {
+    "tiny-f32": W.WORKLOADS["tiny"],
+    "wan-bf16-d128-ragged": W.scaled(W.WORKLOADS["wan"], grid=(4, 12, 30), H=3, name="wan-small"),
+    "cog-bf16-d64-ragged": W.scaled(W.WORKLOADS["cog"], grid=(3, 10, 45), H=4, name="cog-small"),
+    "bf16-d128-blk64": W.scaled(W.Workload("b64", 1, 2, 128, "bf16", (3, 9, 25), 64, 0.99, 1.5,
+                                           0.5, 0.02, 1, 77), name="bf16-d128-b64"),
+    "bf16-d64-blk64": W.Workload("bf16-d64-b64", 2, 2, 64, "bf16", (2, 11, 23), 64, 0.95, 2.0,
+                                 0.5, 0.02, 1, 78),
+    "f32-d128-blk128": W.Workload("f32-d128-b128", 1, 2, 128, "f32", (2, 10, 25), 128, 0.99, 1.5,
+                                  0.5, 0.02, 1, 79),
+    "f32-d64-blk128": W.Workload("f32-d64-b128", 1, 3, 64, "f32", (2, 10, 19), 128, 0.9, 1.5,
+                                 0.5, 0.02, 1, 80),
+}
+
+
+@pytest.mark.parametrize("key", list(SMALL))
+def test_small_pipeline_all_rows(L, key):
+    w = SMALL[key]
+    info = run_case(L, w, w.tau, reuse=min(w.reuse, 3), label=key)
+    assert 0 < info["coverage"] <= 1
+
+
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32"])
+def test_small_tau_one_is_dense(L, key):
+    w = SMALL[key]
+    q, k, v = W.make_inputs(w, device="cuda")
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, want_lse=False)
+    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, 1.0)
+    o = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci)
+    torch.cuda.synchronize()
+    assert L.nnz(rp) == w.B * w.H * w.n_blocks * w.n_blocks
+    o_ref, _ = O.dense_attention(f64(q), f64(k), f64(v), w.N, w.scale)
+    mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
+    tmax, tmean = out_tol(w)
+    assert mx <= tmax and mean <= tmean, (mx, mean)
+
+
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32"])
+def test_select_on_oracle_masses(L, key):
+    # the selection kernel alone, fed the oracle's masses (rounded to fp32 for
+    # both sides), at several thresholds
+    w = SMALL[key]
+    q, k, _ = W.make_inputs(w)
+    m_ref, _ = O.block_masses(q.float().numpy(), k.float().numpy(), w.N, w.block, w.block, w.scale)
+    m32 = m_ref.astype(np.float32)
+    mdev = torch.from_numpy(m32).cuda()
+    n_q = w.n_blocks
+    n_kv = O.num_valid_key_blocks(w.N, w.block)
+    for tau in (0.5, 0.9, 0.95, 0.99, 0.999, 1.0):
+        rp, ci = L.losa_select_blocks(mdev, w.N, w.block, w.block, tau)
+        torch.cuda.synchronize()
+        rp_g = rp.cpu().numpy().astype(np.int64)
+        ci_g = ci[:rp_g[-1]].cpu().numpy().astype(np.int64)
+        m64 = m32.astype(np.float64)
+        details = [O.select_row(m64.reshape(-1, n_q)[r], tau32(tau), n_kv) for r in range(rp_g.size - 1)]
+        cmp = CMP.compare_selection(rp_g, ci_g, details, m64, tau32(tau))
+        assert cmp["ok"], (tau, cmp)
+
+
+def test_select_ties_go_to_smaller_index(L):
+    # equal masses everywhere: the kept prefix is the smallest indices
+    B, H, n, N = 1, 2, 8, 8 * 64
+    m = torch.full((B, H, n, n), 1.0 / n, dtype=torch.float32, device="cuda")
+    rp, ci = L.losa_select_blocks(m, N, 64, 64, 0.5)
+    torch.cuda.synchronize()
+    rp_h = rp.cpu().numpy()
+    assert np.all(np.diff(rp_h) == 4)
+    assert ci[:rp_h[-1]].cpu().numpy().reshape(-1, 4).tolist() == [[0, 1, 2, 3]] * (B * H * n)
+
+
+def test_fwd_edge_case_csr(L):
+    # empty row, single-block row, descending order, out-of-range ids, full row
+    w = SMALL["wan-bf16-d128-ragged"]
+    q, k, v = W.make_inputs(w, device="cuda")
+    n_q = n_k = w.n_blocks
+    R = w.B * w.H * n_q
+    rows = []
+    for r in range(R):
+        kind = r % 5
+        if kind == 0:
+            rows.append([])
+        elif kind == 1:
+            rows.append([r % n_k])
+        elif kind == 2:
+            rows.append(sorted({(r + 3) % n_k, (r + 7) % n_k, n_k - 1}, reverse=True))
+        elif kind == 3:
+            rows.append([-1, 0, n_k + 5, 2])
+        else:
+            rows.append(list(range(n_k)))
+    rp = np.zeros(R + 1, np.int64)
+    for r, seg in enumerate(rows):
+        rp[r + 1] = rp[r] + len(seg)
+    ci = np.array([j for seg in rows for j in seg], np.int64)
+    rp_d = torch.from_numpy(rp.astype(np.int32)).cuda()
+    ci_d = torch.from_numpy(ci.astype(np.int32)).cuda()
+    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp_d, ci_d, want_lse=True)
+    torch.cuda.synchronize()
+    # ids outside [0, n_k) are ignored by contract: drop them for the oracle
+    keep = (ci >= 0) & (ci < n_k)
+    rp_clean = np.concatenate([[0], np.cumsum([np.sum(keep[rp[r]:rp[r + 1]]) for r in range(R)])])
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+                                      rp_clean, ci[keep])
+    mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
+    assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
+    lg = f64(lse)
+    empty_rows = [r for r in range(R) if r % 5 == 0]
+    for r in empty_rows:
+        h, i = divmod(r, n_q)
+        assert np.all(f64(o)[0, h, i * w.block:(i + 1) * w.block] == 0)
+        assert np.all(np.isneginf(lg[0, h, i * w.block:(i + 1) * w.block]))
+    valid = ~np.isneginf(l_ref)
+    assert np.abs(lg[valid] - l_ref[valid]).max() <= LSE_TOL
+
+    # a col_idx shorter than row_ptr claims: row bounds are clamped
+    cut = int(rp[-1]) - 7
+    o2 = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp_d, ci_d[:cut])
+    torch.cuda.synchronize()
+    rp_cut = np.minimum(rp, cut)
+    ci_cut = ci[:cut]
+    keep = (ci_cut >= 0) & (ci_cut < n_k)
+    rp_cut_clean = np.concatenate([[0], np.cumsum([np.sum(keep[rp_cut[r]:rp_cut[r + 1]])
+                                                   for r in range(R)])])
+    o_ref2, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+                                   rp_cut_clean, ci_cut[keep])
+    mx, mean = CMP.output_errors(f64(o2), o_ref2, w.N)
+    assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
+
+
+def test_deterministic(L):
+    w = SMALL["cog-bf16-d64-ragged"]
+    q, k, v = W.make_inputs(w, device="cuda")
+    outs = []
+    for _ in range(2):
+        mass, lse = L.losa_calibrate_mass(q, k, w.N, w.block)
+        rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, w.tau)
+        o = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci)
+        torch.cuda.synchronize()
+        outs.append((mass.clone(), lse.clone(), rp.clone(), ci[:L.nnz(rp)].clone(), o.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+# ----------------------------------------------------------------------------
+# full-size workloads, sampled rows
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan"])
+def test_full_size_sampled(L, key):
+    w = W.WORKLOADS[key]
+    info = run_case(L, w, w.tau, reuse=1, rows=sample_rows(w), label=f"full-{key}")
+    say(f"full-{key}: coverage {info['coverage']:.3f} nnz {info['nnz']}")
+
+
+@pytest.mark.parametrize("alpha", W.SWEEP_ALPHAS)
+def test_density_sweep_sampled(L, alpha):
+    pts = [p for p in W.sweep_points() if p.alpha == alpha]
+    base = pts[0]
+    state = W.make_state(base, device="cuda")
+    q, k, v = W.cast(state, base)
+    N, C = base.N, base.block
+    say(f"sweep alpha={alpha}: calibrate")
+    mass, _ = L.losa_calibrate_mass(q, k, N, C, want_lse=False)
+    rows = sample_rows(base)
+    n_q = base.n_blocks
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    m_ref, _ = O.block_masses(qh, kh, N, C, C, base.scale, rows_subset=rows)
+    flat = m_ref.reshape(-1, n_q)
+    assert np.abs(f64(mass).reshape(-1, n_q)[rows] - flat[rows]).max() <= MASS_TOL
+    prev_cov = 0.0
+    for p in pts:
+        rp, ci = L.losa_select_blocks(mass, N, C, C, p.tau)
+        o = L.losa_sparse_attn_fwd(q, k, v, N, C, C, rp, ci)
+        torch.cuda.synchronize()
+        rp_g = rp.cpu().numpy().astype(np.int64)
+        ci_g = ci[:rp_g[-1]].cpu().numpy().astype(np.int64)
+        cov = rp_g[-1] / (rp_g.size - 1) / n_q
+        say(f"sweep tau={p.tau} alpha={alpha}: coverage {cov:.3f}")
+        assert cov >= prev_cov
+        prev_cov = cov
+        details = [O.select_row(flat[r], tau32(p.tau), n_q) for r in rows]
+        srp, sci = sub_csr(rp_g, ci_g, rows)
+        cmp = CMP.compare_selection(srp, sci, details, flat[rows], tau32(p.tau))
+        assert cmp["ok"], cmp
+        if p.tau >= 1.0:
+            ref, _ = O.sparse_attention(qh, kh, vh, N, C, C, base.scale,
+                                        np.arange(rp_g.size) * n_q,
+                                        np.tile(np.arange(n_q), rp_g.size - 1), rows_subset=rows)
+        else:
+            ref, _ = O.sparse_attention(qh, kh, vh, N, C, C, base.scale, rp_g, ci_g,
+                                        rows_subset=rows)
+        qrows = np.concatenate([np.arange(i * C, min((i + 1) * C, N)) + (r // n_q) * base.N_pad
+                                for r in rows for i in [r % n_q]])
+        err = np.abs(f64(o).reshape(-1, base.d)[qrows] - ref.reshape(-1, base.d)[qrows])
+        assert err.max() <= OUT_MAX and err.mean() <= OUT_MEAN, (p.tau, err.max(), err.mean())
