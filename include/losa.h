@@ -19,7 +19,7 @@
  *   blocks per head (the partition of Sec. 3.1); row r = (b*H + h)*n_q + i
  *   addresses query block i of head h in batch b (a classifier-free-guidance
  *   branch is simply another b).
- * - `scale` multiplies Q K^T before the softmax; the method uses 1/sqrt(d).
+ * - `scale` (> 0) multiplies Q K^T before the softmax; the method uses 1/sqrt(d).
  * - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
  *   asynchronously; outputs are valid once the stream has reached that point.
  * - Validation is synchronous and happens before any HIP call: on an error
@@ -115,15 +115,17 @@ losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block
  *
  * q, k, v     [B][H][N_pad][d] of `dtype`.
  * row_ptr     int32 [B*H*n_q + 1]; col_idx int32 [col_idx_len].  A row's ids
- *             must be distinct (any order); ids outside [0, n_k) are ignored;
- *             row bounds are clamped to [0, col_idx_len], so a malformed CSR
- *             cannot make the kernel read outside col_idx.
+ *             may come in any order; a repeated id counts once (K(q) is a set);
+ *             ids outside [0, n_k) are ignored; row bounds are clamped to
+ *             [0, col_idx_len], so a malformed CSR cannot make the kernel read
+ *             outside col_idx.  n_k <= 4096, else LOSA_ERR_UNSUPPORTED.
  * o           out, [B][H][N_pad][d] of `dtype`.  Rows with an empty key set and
  *             padding rows are 0.
  * lse         out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp over
  *             K(q) of the scaled scores; -inf for empty or padding rows.
  * workspace   >= losa_workspace_bytes(2, ...) bytes (bf16: a transposed copy
- *             of V, B*H*N_pad*d*2 bytes; f32: none).
+ *             of V in the kernel's tile layout, B*H*N_pad*d*2 bytes, rewritten
+ *             by every call; f32: none).
  * Arithmetic (bf16): Q K^T and P V on bf16 matrix cores with fp32
  * accumulation, softmax in fp32, P rounded to bf16 for the P V product, O
  * rounded to bf16 once at the end.  f32: fp32 throughout.

@@ -26,6 +26,9 @@ COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # keep the compiler from emitting packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in arch VGPRs: the softmax works on the score accumulators
+    # directly instead of copying them out of AGPRs
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", INCLUDE, "-I", CSRC,
     "-Wno-unused-command-line-argument",
 ]
@@ -47,6 +50,20 @@ def _run(cmd):
     return out
 
 
+def _check_stubs(lib: str) -> None:
+    """Fail if a kernel's host launch stub is missing from the library.
+
+    The host compiler pass can drop a kernel template instantiation without a
+    diagnostic; the library then links but cannot be loaded."""
+    p = subprocess.run(["nm", "-D", "--undefined-only", lib], stdout=subprocess.PIPE,
+                       stderr=subprocess.STDOUT, text=True)
+    if p.returncode != 0:
+        return  # no nm: the load test catches the same problem
+    missing = [ln.split()[-1] for ln in p.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        raise RuntimeError("kernel launch stubs missing from the host build: " + ", ".join(missing))
+
+
 def build(verbose: bool = False, jobs: int | None = None) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     hipcc = _hipcc()
@@ -66,6 +83,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
                 print(o)
     tmp = OUT + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    _check_stubs(tmp)
     os.replace(tmp, OUT)
     return OUT
 

@@ -96,7 +96,8 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
   Shape s;
   losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
   if (st != LOSA_OK) return st;
-  if (!std::isfinite(scale)) return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite and > 0");
   if (!aligned16(q) || !aligned16(k) || !aligned16(mass) || (lse && !aligned16(lse)))
     return fail(LOSA_ERR_ALIGNMENT, "tensor pointers must be 16-byte aligned");
   st = check_supported(dtype, s);
@@ -159,12 +160,16 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
   Shape s;
   losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
   if (st != LOSA_OK) return st;
-  if (!std::isfinite(scale)) return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite and > 0");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
       (lse && !aligned16(lse)) || !aligned16(row_ptr) || (col_idx && !aligned16(col_idx)))
     return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
   st = check_supported(dtype, s);
   if (st != LOSA_OK) return st;
+  if (s.n_k > losa::kSparseFwdMaxNk)
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per head exceeds %d", s.n_k,
+                losa::kSparseFwdMaxNk);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (dtype == LOSA_DTYPE_BF16) {
     const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d);

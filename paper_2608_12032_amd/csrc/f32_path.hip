@@ -7,7 +7,8 @@
 // by every thread as broadcasts.  Masking and padding follow the bf16 kernels:
 // keys >= N never enter a softmax, query rows >= N get O = 0 and lse = -inf,
 // and so do rows whose key set is empty; col_idx entries outside [0, n_k) are
-// ignored and row bounds are clamped to [0, col_idx_len].
+// ignored, a repeated entry counts once (the row's ids are flagged in LDS and
+// walked in ascending order), and row bounds are clamped to [0, col_idx_len].
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -52,12 +53,19 @@ __global__ void __launch_bounds__(BLK)
   }
   float m = kNegBig, l = 0.f;
 
+  __shared__ uint8_t flag[kSparseFwdMaxNk];
+  for (int j = t; j < n_k; j += BLK) flag[j] = 0;
+  __syncthreads();
   int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
   e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
   e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
-  for (int64_t e = e0; e < e1; ++e) {
+  for (int64_t e = e0 + t; e < e1; e += BLK) {
     const int j = col_idx[e];
-    if (j < 0 || j >= n_k) continue;
+    if (j >= 0 && j < n_k) flag[j] = 1;
+  }
+  __syncthreads();
+  for (int j = 0; j < n_k; ++j) {
+    if (!flag[j]) continue;  // the same LDS value for every thread
     const int kvalid = min(BLK, N - j * BLK);
     for (int c0 = 0; c0 < kvalid; c0 += CK) {
       __syncthreads();

@@ -40,4 +40,8 @@ hipError_t launch_sparse_fwd_f32(int d, int blk, const void* q, const void* k, c
                                  void* o, float* lse, hipStream_t stream);
 size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d);
 
+// Largest n_k (key blocks per head) the sparse forward kernels accept: each
+// workgroup keeps one flag per key block of its row in LDS.
+constexpr int kSparseFwdMaxNk = 4096;
+
 }  // namespace losa

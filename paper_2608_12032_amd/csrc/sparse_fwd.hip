@@ -1,19 +1,24 @@
 // Frozen-support block-sparse attention forward (Sec. 4.2, Eq. (4)), bf16 in,
 // fp32 accumulation, on gfx950 MFMA.
 //
-// One workgroup owns one CSR row r = (b*H + h)*n_q + i, i.e. the BLK query rows
-// of query block i, and walks only the key blocks listed for it.  Each of its
-// BLK/32 waves owns 32 query rows.
+// Work unit.  One workgroup owns one CSR row r = (b*H + h)*n_q + i: the BLK
+// query rows of query block i, 32 per wave (BLK/32 waves, one per SIMD for
+// BLK = 128), and walks only the key blocks the row retains.  Two workgroups
+// share a CU, so each SIMD runs two independent waves: while one waits at its
+// workgroup barrier the other keeps the matrix core busy.  The workgroup first
+// turns its CSR entries into a sorted list of distinct valid block ids in LDS
+// (per-block flags, then a ballot compaction), which realises Eq. (4)'s set
+// semantics exactly: a repeated id counts once, ids outside [0, n_k) are
+// dropped.
 //
-// Orientation.  Per 32-key sub-block the wave computes S^T = K Q^T with
+// Orientation.  Per 32-key sub-tile the wave computes S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = the wave's Q^T held in
-// registers).  In the 32x32 accumulator layout a lane holds 16 scores of ONE
-// query (column = lane % 32), so the online softmax (running max m, running
-// sum l) is in-lane, plus one exchange with lane ^ 32 which holds the other
-// keys of the same query.  The exponentiated scores are already laid out as
-// the B operand of O^T = V^T P^T, and the O^T accumulator again keeps one
-// query per lane, so the per-query rescale by exp2(m_old - m_new) and the
-// final 1/l are in-lane too.
+// registers).  In the 32x32 accumulator a lane holds 16 scores of ONE query
+// (column = lane % 32), so the online softmax (running max, running sum) is
+// in-lane plus one exchange with lane ^ 32, which holds the other keys of the
+// same query.  The exponentiated scores are already laid out as the B operand
+// of O^T = V^T P^T, and the O^T accumulator again keeps one query per lane, so
+// the per-query rescale and the final 1/l are in-lane too.
 //
 // Key order inside a 16-key MFMA step.  The B operand P^T of lane group g
 // (lanes 32g..32g+31) holds, in register element e, the key
@@ -23,25 +28,40 @@
 // therefore stores, within every group of 16 keys, positions 4..7 and 8..11
 // swapped (an involution), so each lane's 8 keys are 16 contiguous bytes.
 //
-// Staging.  K tiles ([BLK keys][D]) and V^T tiles ([D][BLK keys]) are copied
-// HBM -> LDS with 16-byte buffer loads that write LDS directly (no register
-// round trip).  16-byte chunks are XOR-swizzled by row so that the MFMA operand
-// reads (32 rows, one chunk column) hit distinct banks.  The K buffer is
-// refilled as soon as all waves have finished S for the current tile, the V
-// buffer as soon as P V is done, so the next tile's loads overlap the softmax
-// and the P V product.  Two workgroups share a CU (64 KiB of LDS each).
+// Streaming.  The row's keys are a stream of 32-key sub-tiles (NS = BLK/32 per
+// key block).  K and V^T sub-tiles pass through two rings of kRing LDS slots,
+// filled by 16-byte buffer loads that write LDS directly.  Sub-iteration s
+// reads K sub-tile s+1 (scores of the next sub-tile) and V^T sub-tile s-1
+// (P V of the previous one); after the barrier that opens it, the slots that
+// sub-iteration s-1 finished with are refilled with K sub-tile s+kRing and V^T
+// sub-tile s+kRing-2, both needed kRing-1 sub-iterations later.  Inside a
+// sub-iteration the matrix cores alternate the next scores with P V of the
+// previous sub-tile while the VALU exponentiates the current one; the
+// instruction interleave is fixed with sched_group_barrier.
+//
+// LDS images.  A K sub-tile is 32 rows of D bf16, row-major, 16-byte chunks
+// XOR-swizzled by 256-byte line; V^T is kept in global memory already in the
+// LDS image of its sub-tiles (written by the transpose kernel), so its loads
+// are plain contiguous copies.  Both swizzles make the 16 rows read by one
+// 16-lane group of an operand read land in distinct banks.
 //
 // Padding.  Keys >= N get score -inf (only the ragged last block needs it).
 // Query rows >= N are written as 0 with lse = -inf; so are rows with an empty
-// key set.  Entries of col_idx outside [0, n_k) contribute nothing, and row
-// bounds are clamped to [0, col_idx_len], so a corrupt CSR cannot read out of
-// bounds.
+// key set.  Row bounds are clamped to [0, col_idx_len], so a malformed CSR
+// cannot make the kernel read outside col_idx.
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace losa {
 
 namespace {
+
+// Entries of the in-LDS block list.
+constexpr int kMaxList = kSparseFwdMaxNk;
+// Sub-tile slots per operand ring.
+constexpr int kRing = 4;
 
 // Position <-> key permutation inside a group of 16 keys (swap of quads 1, 2).
 __device__ __forceinline__ int perm16(int p) {
@@ -52,67 +72,200 @@ __device__ __forceinline__ int perm16(int p) {
 
 template <int D, int BLK>
 struct FwdCfg {
-  static constexpr int NW = BLK / 32;               // waves per workgroup
-  static constexpr int NT = NW * 64;                // threads
-  static constexpr int KS = D / 16;                 // k-steps of S^T = K Q^T
-  static constexpr int KB = BLK / 32;               // 32-key sub-blocks per tile
-  static constexpr int PS = BLK / 16;               // k-steps of O^T = V^T P^T
-  static constexpr int DB = D / 32;                 // 32-row d sub-blocks
-  static constexpr int KROW = D * 2;                // bytes of one K row in LDS
-  static constexpr int KCH = D / 8;                 // 16-byte chunks per K row
-  static constexpr int VROW = BLK * 2;              // bytes of one V^T row in LDS
-  static constexpr int VCH = BLK / 8;               // 16-byte chunks per V^T row
-  static constexpr int TILE = BLK * D * 2;          // bytes of a K or V^T tile
-  static constexpr int LOADS = TILE / (1024 * NW);  // wave loads per tile per wave
-  static_assert(TILE % (1024 * NW) == 0, "tile must split into whole wave loads");
-  static_assert(KCH >= 8 && VCH >= 8, "swizzle needs >= 8 chunks per row");
+  static constexpr int NW = BLK / 32;                // waves per workgroup
+  static constexpr int NT = NW * 64;                 // threads
+  static constexpr int KS = D / 16;                  // k-steps of S^T = K Q^T
+  static constexpr int DB = D / 32;                  // 32-row d sub-blocks of O^T
+  static constexpr int NS = BLK / 32;                // 32-key sub-tiles per key block
+  static constexpr int R = kRing;                    // slots per ring
+  static constexpr int BPI = R / NS;                 // key blocks per unrolled loop pass
+  static constexpr int SUB = 32 * D * 2;             // bytes of a K or V^T sub-tile
+  static constexpr int RING = R * SUB;               // bytes of one ring
+  static constexpr int LPW = SUB / (1024 * NW);      // 1 KiB wave loads per sub-tile
+  static constexpr int KROW = D * 2;                 // bytes of a K row
+  static constexpr int KCPR = KROW / 16;             // 16-byte chunks per K row
+  static constexpr int KRPL = 256 / KROW;            // K rows per 256-byte line
+  static constexpr int VDB = 32 * 64;                // bytes of 32 V^T rows in a sub-tile
+  static_assert(SUB % (1024 * NW) == 0, "sub-tile must split into whole wave loads");
+  static_assert(R % NS == 0 && R >= 4 && (R & 1) == 0, "ring holds whole key blocks");
+  static_assert(KS == 2 * DB, "QK and PV steps alternate one to one");
+  static_assert(2 * RING >= kMaxList + 4 * NW, "list-building scratch fits the rings");
 };
 
-// Issue the direct loads of K tile j (rows j*BLK.., all D) into LDS.
+// Swizzled chunk of K chunk c in sub-tile row `row`.
 template <int D, int BLK>
-__device__ __forceinline__ void issue_k_tile(char* Ks, __amdgpu_buffer_rsrc_t rs, int j, int w,
-                                             int lane) {
+__device__ __forceinline__ int kswz(int row, int c) {
   using C = FwdCfg<D, BLK>;
+  return c ^ ((row / C::KRPL) % C::KCPR);
+}
+
+// NL consecutive 1 KiB direct loads of one wave into LDS at dst: load u moves
+// 16 bytes per lane from offs[u] (or voff + 1024*u when offs is null) plus the
+// wave-uniform sbase.
+template <int NL>
+__device__ __forceinline__ void wave_loads(char* dst, __amdgpu_buffer_rsrc_t rs,
+                                           const uint32_t* offs, uint32_t voff, uint32_t sbase) {
 #pragma unroll
-  for (int u = 0; u < C::LOADS; ++u) {
-    const int base = (w * C::LOADS + u) * 1024;
-    const int o = base + lane * 16;
-    const int row = o / C::KROW;
-    const int pch = (o % C::KROW) >> 4;
-    const int c = pch ^ (row % C::KCH);
-    const uint32_t voff = (uint32_t)(((j * BLK + row) * D + c * 8) * 2);
-    load_lds_16(rs, Ks + base, voff);
+  for (int u = 0; u < NL; ++u)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (__attribute__((address_space(3))) void*)(dst + u * 1024), 16,
+        offs ? offs[u] : voff + u * 1024, sbase, 0, 0);
+}
+
+// max / sum of a value and the one held by lane ^ 32 (v_permlane32_swap gives
+// each lane the pair {own, partner} in some order; max and + do not care).
+__device__ __forceinline__ float max_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
+
+// 16-byte LDS read at byte address `addr` (+ a compile-time immediate).
+__device__ __forceinline__ bf16x8_t lds_read16(uint32_t addr) {
+  return *reinterpret_cast<lds_bf16x8_t*>(addr);
+}
+
+// Keep a per-lane LDS base address opaque inside the loop, so that every
+// operand read stays "base + immediate" instead of the compiler hoisting one
+// precomputed address per (slot, k-step) into its own register.
+__device__ __forceinline__ void launder(uint32_t& x) { asm volatile("" : "+v"(x)); }
+
+// Unpipelined S^T = K Q^T of one sub-tile (QK) and/or O^T += V^T P^T of one
+// sub-tile (PV); the prologue and the drain of the pipeline.  ka[st] is this
+// lane's LDS address of its chunk for k-step st in K slot 0, va[st] the same
+// in V^T slot 0; kimm / vimm select the slot.
+template <int D, int BLK, bool QK, bool PV>
+__device__ __forceinline__ void mfma_pair(const uint32_t* ka, uint32_t kimm, const bf16x8_t* qreg,
+                                          f32x16_t& snext, const uint32_t* va, uint32_t vimm,
+                                          const bf16x8_t* pprev, f32x16_t* o) {
+  using C = FwdCfg<D, BLK>;
+  constexpr int NPV = 2 * C::DB;
+#pragma unroll
+  for (int i = 0; i < C::KS; ++i) {
+    if constexpr (QK) {
+      const bf16x8_t a = lds_read16(ka[i] + kimm);
+      snext = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[i], i == 0 ? f32x16_t{} : snext, 0,
+                                                      0, 0);
+    }
+    if constexpr (PV) {
+      if (i < NPV) {
+        const int st = i / C::DB, db = i % C::DB;
+        const bf16x8_t a = lds_read16(va[st] + vimm + db * C::VDB);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pprev[st], o[db], 0, 0, 0);
+      }
+    }
   }
 }
 
-// Issue the direct loads of V^T tile j (all D rows, keys j*BLK..) into LDS.
-template <int D, int BLK>
-__device__ __forceinline__ void issue_v_tile(char* Vs, __amdgpu_buffer_rsrc_t rs, int j,
-                                             int n_pad, int w, int lane) {
+// One pipelined sub-iteration, issued in a fixed order: NM = KS + 2*DB MFMAs
+// alternate between S^T(next) = K Q^T (a KS-long dependent chain) and
+// O^T += V^T P^T(prev) (2 k-steps x DB independent chains); each MFMA's LDS
+// operand is read NPRE MFMAs ahead from a small register ring, and after each
+// MFMA the VALU exponentiates 16/NM elements of the current scores (fp32 sum
+// and bf16 pack).  sched_group_barrier fixes this order, so the LDS latency
+// and the softmax both hide behind the matrix cores.
+template <int D, int BLK, int NPRE>
+__device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm,
+                                               const bf16x8_t* qreg, f32x16_t& snext,
+                                               const uint32_t* va, uint32_t vimm,
+                                               const bf16x8_t* pprev, f32x16_t* o, f32x16_t& cur,
+                                               float scale_log2, float m_run, bf16x8_t* pcur) {
   using C = FwdCfg<D, BLK>;
+  constexpr int NM = C::KS + 2 * C::DB;
+  constexpr int EPS = 16 / NM;  // softmax elements per MFMA
+  static_assert(EPS * NM == 16, "softmax elements split evenly over the MFMAs");
+  auto read_op = [&](int i) -> bf16x8_t {
+    if ((i & 1) == 0) return lds_read16(ka[i >> 1] + kimm);
+    const int st = (i >> 1) / C::DB, db = (i >> 1) % C::DB;
+    return lds_read16(va[st] + vimm + db * C::VDB);
+  };
+  bf16x8_t ring[NPRE];
 #pragma unroll
-  for (int u = 0; u < C::LOADS; ++u) {
-    const int base = (w * C::LOADS + u) * 1024;
-    const int o = base + lane * 16;
-    const int row = o / C::VROW;
-    const int pch = (o % C::VROW) >> 4;
-    const int c = pch ^ (row % C::VCH);
-    const uint32_t voff = (uint32_t)(((size_t)row * n_pad + j * BLK + c * 8) * 2);
-    load_lds_16(rs, Vs + base, voff);
+  for (int i = 0; i < NPRE; ++i) ring[i] = read_op(i);
+  float ls0 = 0.f, ls1 = 0.f;
+  f32x8_t p;
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    const bf16x8_t a = ring[i % NPRE];
+    if ((i & 1) == 0) {
+      const int st = i >> 1;
+      snext = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], st == 0 ? f32x16_t{} : snext,
+                                                      0, 0, 0);
+    } else {
+      const int st = (i >> 1) / C::DB, db = (i >> 1) % C::DB;
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pprev[st], o[db], 0, 0, 0);
+    }
+    if (i + NPRE < NM) ring[i % NPRE] = read_op(i + NPRE);
+#pragma unroll
+    for (int u = 0; u < EPS; ++u) {
+      const int e = i * EPS + u;
+      const float pe = fast_exp2(__builtin_fmaf(cur[e], scale_log2, -m_run));
+      p[e & 7] = pe;
+      if (e & 1) ls1 += pe; else ls0 += pe;
+      if ((e & 7) == 7) pcur[e >> 3] = __builtin_convertvector(p, bf16x8_t);
+    }
+  }
+  // fixed issue order: the NPRE lead reads, then per MFMA the next read and
+  // the softmax work of its elements
+  __builtin_amdgcn_sched_group_barrier(0x100, NPRE, 0);
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i + NPRE < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 3 * EPS, 0);
+  }
+  // pin the softmax results here: otherwise the compiler sinks the exp2 work
+  // next to its consumers in the following sub-iteration, out of the shadow
+  // of these MFMAs
+  float ls = ls0 + ls1;
+  asm volatile("" : "+v"(ls), "+v"(pcur[0]), "+v"(pcur[1]));
+  return ls;
+}
+
+// Raw-score maximum of a 32-key sub-tile for this lane's query (both halves).
+__device__ __forceinline__ float sub_max(const f32x16_t& s) {
+  float m = s[0];
+#pragma unroll
+  for (int t = 1; t < 16; ++t) m = fmaxf(m, s[t]);
+  return max_with_partner(m);
+}
+
+// Scores of sub-tile `part`'s keys at or beyond kvalid (block-relative) -> -inf.
+__device__ __forceinline__ void mask_sub(f32x16_t& s, int part, int kvalid, int g) {
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    const int key = part * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
+    if (key >= kvalid) s[t] = -INFINITY;
   }
 }
 
+// Lazy rescale threshold (log2 units): the running max used for exp2 is only
+// raised when a sub-tile's max exceeds it by more than this, so probabilities
+// stay <= 2^8 and the O rescale is skipped on most sub-tiles.
+constexpr float kRescaleThreshold = 8.0f;
+
 template <int D, int BLK>
-__global__ void __launch_bounds__(BLK * 2, 2)
+__global__ void __launch_bounds__(BLK * 2)
+    __attribute__((amdgpu_waves_per_eu(BLK == 128 ? 2 : 1)))
     sparse_fwd_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                            const __bf16* __restrict__ Vt, const int32_t* __restrict__ row_ptr,
                            const int32_t* __restrict__ col_idx, int64_t col_len,
                            __bf16* __restrict__ O, float* __restrict__ lse, int rows_total,
                            int n_q, int n_k, int N, int n_pad, float scale_log2) {
   using C = FwdCfg<D, BLK>;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * C::TILE];
-  char* Ks = smem;
-  char* Vs = smem + C::TILE;
+  constexpr int NS = C::NS;
+  constexpr int R = C::R;
+  constexpr int BPI = C::BPI;
+  // K ring at smem, V^T ring at smem + RING; slot x at + x*SUB
+  __shared__ __attribute__((aligned(1024))) char smem[2 * C::RING];
+  __shared__ uint16_t list[kMaxList];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -122,152 +275,213 @@ __global__ void __launch_bounds__(BLK * 2, 2)
 
   const int r = xcd_remap(blockIdx.x, rows_total);
   const int bh = r / n_q;
-  const int i = r - bh * n_q;
+  const int qb = r - bh * n_q;
   const size_t head = (size_t)bh * n_pad * D;
   const uint32_t head_bytes = (uint32_t)((size_t)n_pad * D * 2);
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(K + head, head_bytes);
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(Vt + head, head_bytes);
 
-  int64_t e0 = row_ptr[r];
-  int64_t e1 = row_ptr[r + 1];
-  e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
-  e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
+  // ---- the row's distinct valid key blocks, ascending ---------------------
+  // (flags and per-wave counts live in the rings, unused until the first load)
+  int nb = 0;
+  {
+    uint8_t* const flag = reinterpret_cast<uint8_t*>(smem);
+    int* const wcount = reinterpret_cast<int*>(smem + kMaxList);
+    for (int j = tid; j < n_k; j += C::NT) flag[j] = 0;
+    __syncthreads();
+    int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
+    for (int64_t e = e0 + tid; e < e1; e += C::NT) {
+      const int j = col_idx[e];
+      if (j >= 0 && j < n_k) flag[j] = 1;
+    }
+    __syncthreads();
+    for (int c0 = 0; c0 < n_k; c0 += C::NT) {
+      const int j = c0 + tid;
+      const bool f = (j < n_k) && flag[j] != 0;
+      const uint64_t bal = __ballot(f);
+      const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+      if (lane == 0) wcount[w] = __popcll(bal);
+      __syncthreads();
+      int before = 0, total = 0;
+#pragma unroll
+      for (int x = 0; x < C::NW; ++x) {
+        const int c = wcount[x];
+        before += (x < w) ? c : 0;
+        total += c;
+      }
+      if (f) list[nb + before + below] = (uint16_t)j;
+      nb += total;
+      __syncthreads();
+    }
+    nb = __builtin_amdgcn_readfirstlane(nb);
+  }
+  const int S = nb * NS;  // sub-tiles in the stream
 
   // this lane's query row and its Q^T operand (8 bf16 per k-step)
-  const int qrow = i * BLK + w * 32 + l32;
+  const int qrow = qb * BLK + w * 32 + l32;
   bf16x8_t qreg[C::KS];
   {
     const bf16x8_t* qp = reinterpret_cast<const bf16x8_t*>(Q + head + (size_t)qrow * D);
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[s] = qp[2 * s + g];
+    for (int st = 0; st < C::KS; ++st) qreg[st] = qp[2 * st + g];
   }
+  // per-lane LDS addresses of the operand reads in K slot 0 / V^T slot 0; the
+  // slot and the d sub-block are immediates
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+  uint32_t ka[C::KS], va[2];
+#pragma unroll
+  for (int st = 0; st < C::KS; ++st)
+    ka[st] = lds0 + l32 * C::KROW + (kswz<D, BLK>(l32, 2 * st + g) << 4);
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+    va[st] = lds0 + C::RING + (l32 >> 2) * 256 +
+             (((l32 & 3) << 2) + ((2 * st + g) ^ ((l32 >> 2) & 3))) * 16;
+  // per-lane global offsets of the direct loads (LDS position o of a K sub-tile
+  // holds row o / KROW, chunk kswz(row, (o % KROW) / 16); V^T is stored as the
+  // LDS image)
+  uint32_t koffs[C::LPW];
+#pragma unroll
+  for (int u = 0; u < C::LPW; ++u) {
+    const int o = (w * C::LPW + u) * 1024 + lane * 16;
+    const int row = o / C::KROW;
+    koffs[u] = (uint32_t)(row * C::KROW + (kswz<D, BLK>(row, (o % C::KROW) >> 4) << 4));
+  }
+  const uint32_t voff0 = (uint32_t)(w * C::LPW * 1024 + lane * 16);
 
-  // per-lane LDS byte offsets of the operand reads (row part added per sub-block)
-  const int ksw = l32 % C::KCH;
-  const int vsw = l32 % C::VCH;
+  // key sub-tile (block j, part) -> K slot x / V^T slot x
+  auto load_k = [&](int x, int j, int part) {
+    wave_loads<C::LPW>(smem + x * C::SUB + w * C::LPW * 1024, krs, koffs, 0,
+                       (uint32_t)((j * BLK + part * 32) * C::KROW));
+  };
+  auto load_v = [&](int x, int j, int part) {
+    wave_loads<C::LPW>(smem + C::RING + x * C::SUB + w * C::LPW * 1024, vrs, nullptr, voff0,
+                       (uint32_t)((j * NS + part) * C::SUB));
+  };
+  // list entry x as a scalar, clamped into the list
+  auto block_at = [&](int x) -> int {
+    return __builtin_amdgcn_readfirstlane((int)list[x < nb ? x : nb - 1]);
+  };
 
   f32x16_t oacc[C::DB];
 #pragma unroll
-  for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-    for (int t = 0; t < 16; ++t) oacc[db][t] = 0.f;
-  float m_run = kNegBig;
-  float l_run = 0.f;
+  for (int db = 0; db < C::DB; ++db) oacc[db] = f32x16_t{};
+  float m_run = kNegBig;  // max used for exp2 (scaled units)
+  float l_run = 0.f;      // this lane's share of the row sum
+  f32x16_t sc[2];         // raw scores of the sub-tiles with even / odd index
+  bf16x8_t pb[2][2];      // bf16 probabilities of the sub-tiles with even / odd index
 
-  auto block_of = [&](int64_t e) -> int {
-    const int j = __builtin_amdgcn_readfirstlane(col_idx[e]);
-    return j;
-  };
+  if (S > 0) {
+    int jc[BPI], jn[BPI];  // blocks of this loop pass's sub-tiles and the next pass's
+    // prologue: K sub-tiles 0..R-1, V^T sub-tiles 0..R-3; zero V^T slot R-1
+    // and the probabilities of "sub-tile -1"; scores of sub-tile 0
+#pragma unroll
+    for (int x = 0; x < BPI; ++x) {
+      jc[x] = block_at(x);
+      jn[x] = block_at(BPI + x);
+    }
+#pragma unroll
+    for (int y = 0; y < R; ++y) {
+      const int jy = (y / NS < BPI) ? jc[y / NS] : jn[y / NS - BPI];
+      if (y < S) load_k(y, jy, y % NS);
+      if (y < R - 2 && y < S) load_v(y, jy, y % NS);
+    }
+    for (int x = tid * 16; x < C::SUB; x += C::NT * 16)
+      *reinterpret_cast<f32x4_t*>(smem + C::RING + (R - 1) * C::SUB + x) = f32x4_t{};
+#pragma unroll
+    for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+      for (int st = 0; st < 2; ++st) pb[a2][st] = bf16x8_t{};
+    wait_vm_barrier<0>();
+    mfma_pair<D, BLK, true, false>(ka, 0, qreg, sc[0], va, 0, pb[1], oacc);
 
-  int j_cur = 0;
-  if (e0 < e1) {
-    j_cur = block_of(e0);
-    const int jl = (j_cur >= 0 && j_cur < n_k) ? j_cur : 0;
-    issue_k_tile<D, BLK>(Ks, krs, jl, w, lane);
-    issue_v_tile<D, BLK>(Vs, vrs, jl, n_pad, w, lane);
-  }
+    // Sub-iteration s = R*u + H (H static).  On entry the raw scores of s are
+    // in sc[H & 1] and the probabilities of s-1 in pb[(H + 1) & 1].  The
+    // matrix cores compute the scores of s+1 (K slot (H+1) % R) alternating
+    // with P V of s-1 (V^T slot (H-1) % R); the VALU exponentiates s.  The
+    // lazy O rescale decided for s is applied after P V(s-1), before P V(s).
+    // The scores computed for sub-tile S (after the last) are never used; the
+    // first P V multiplies zero probabilities with the zeroed slot.
+    auto sub_iter = [&](auto hh, int u) {
+      constexpr int H = decltype(hh)::value;
+      const int s = R * u + H;
+      f32x16_t& cur = sc[H & 1];
+      f32x16_t& nxt = sc[(H + 1) & 1];
+#pragma unroll
+      for (int st = 0; st < C::KS; ++st) launder(ka[st]);
+      launder(va[0]);
+      launder(va[1]);
+      // K sub-tile s+1 and V^T sub-tile s-1 (loaded R-1 sub-iterations ago)
+      // have landed for every wave, and every wave is done with sub-iteration
+      // s-1; loads of later passes may still be in flight unless the stream
+      // ends within them (then some were not issued and the count is off)
+      if (s - 1 + R < S) wait_vm_barrier<(R - 2) * 2 * C::LPW>(); else wait_vm_barrier<0>();
+      // refill: K slot H <- K sub-tile s+R, V^T slot (H+R-2) % R <- sub-tile s+R-2
+      if (s + R < S) load_k(H, jn[H / NS], H % NS);
+      if (s + R - 2 < S) {
+        constexpr int HV = H + R - 2;  // pass-relative index of sub-tile s+R-2
+        const int jv = (HV < R) ? jc[(HV < R ? HV : 0) / NS] : jn[(HV < R ? 0 : HV - R) / NS];
+        load_v(HV % R, jv, HV % NS);
+      }
+      // ragged last key block: mask the keys >= N of this sub-tile
+      const int kvb = N - jc[H / NS] * BLK;
+      if (kvb < (H % NS + 1) * 32) mask_sub(cur, H % NS, kvb, g);
+      // lazy rescale decision for s (wave-uniform)
+      const float ms = sub_max(cur) * scale_log2;
+      const bool resc = __ballot(ms > m_run + kRescaleThreshold) != 0;
+      float alpha = 1.f;
+      if (resc) {
+        const float m_new = fmaxf(m_run, ms);
+        alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+      }
+      l_run += pipeline_step<D, BLK, 4>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
+                                        ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc, cur,
+                                        scale_log2, m_run, pb[H & 1]);
+      if (resc) {
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) oacc[db] *= alpha;
+      }
+    };
 
-  for (int64_t e = e0; e < e1; ++e) {
-    const bool has_next = (e + 1 < e1);
-    const int j_next = has_next ? block_of(e + 1) : 0;
-    const bool j_ok = (j_cur >= 0 && j_cur < n_k);
-    // keys of this tile that are real (< N); all masked for an invalid index
-    const int kvalid = j_ok ? min(BLK, N - j_cur * BLK) : 0;
-
-    // ---- S^T = K Q^T ------------------------------------------------------
-    wait_vm_barrier<C::LOADS>();  // K(e) landed in LDS for every wave
-    f32x16_t sacc[C::KB];
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    static_assert(R == 4, "loop body written for a ring of 4");
+    for (int u = 0;; ++u) {
+      // block ids of the pass after next: the LDS read completes at the next
+      // barrier and is consumed at the end of this pass
+      int jf[BPI];
 #pragma unroll
-    for (int kb = 0; kb < C::KB; ++kb)
+      for (int x = 0; x < BPI; ++x) {
+        const int xi = (u + 2) * BPI + x;
+        jf[x] = (int)list[xi < nb ? xi : nb - 1];
+      }
+      sub_iter(I0{}, u);
+      sub_iter(I1{}, u);
+      if constexpr (NS == 2) {
+        if (R * u + 2 >= S) break;
+      }
+      sub_iter(I2{}, u);
+      sub_iter(I3{}, u);
+      if (R * (u + 1) >= S) break;
 #pragma unroll
-      for (int t = 0; t < 16; ++t) sacc[kb][t] = 0.f;
-#pragma unroll
-    for (int s = 0; s < C::KS; ++s) {
-      const int off = (((2 * s + g) ^ ksw) << 4);
-#pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb) {
-        const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(Ks + (kb * 32 + l32) * C::KROW + off);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[s], sacc[kb], 0, 0, 0);
+      for (int x = 0; x < BPI; ++x) {
+        jc[x] = jn[x];
+        jn[x] = __builtin_amdgcn_readfirstlane(jf[x]);
       }
     }
-    lds_read_barrier();  // every wave is done reading Ks
-    if (has_next) {
-      const int jl = (j_next >= 0 && j_next < n_k) ? j_next : 0;
-      issue_k_tile<D, BLK>(Ks, krs, jl, w, lane);
-    }
-
-    // ---- online softmax (log2 domain) -------------------------------------
-    float mx = m_run;
-    if (kvalid >= BLK) {
-#pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          const float x = sacc[kb][t] * scale_log2;
-          sacc[kb][t] = x;
-          mx = fmaxf(mx, x);
-        }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          const int key = kb * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
-          const float x = key < kvalid ? sacc[kb][t] * scale_log2 : -INFINITY;
-          sacc[kb][t] = x;
-          mx = fmaxf(mx, x);
-        }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float alpha = fast_exp2(m_run - mx);
-    m_run = mx;
-    float lsum = 0.f;
-    bf16x8_t preg[C::PS];
-#pragma unroll
-    for (int s = 0; s < C::PS; ++s) {
-      const int kb = s >> 1;
-      const int h = (s & 1) * 8;
-      f32x8_t p;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        p[t] = fast_exp2(sacc[kb][h + t] - mx);
-        lsum += p[t];
-      }
-      preg[s] = __builtin_convertvector(p, bf16x8_t);
-    }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-      for (int t = 0; t < 16; ++t) oacc[db][t] *= alpha;
-
-    // ---- O^T += V^T P^T ---------------------------------------------------
-    if (has_next) {
-      wait_vm_barrier<C::LOADS>();  // V(e) landed; K(e+1) may still be in flight
-    } else {
-      wait_vm_barrier<0>();
-    }
-#pragma unroll
-    for (int s = 0; s < C::PS; ++s) {
-      const int off = (((2 * s + g) ^ vsw) << 4);
-#pragma unroll
-      for (int db = 0; db < C::DB; ++db) {
-        const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(Vs + (db * 32 + l32) * C::VROW + off);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, preg[s], oacc[db], 0, 0, 0);
-      }
-    }
-    lds_read_barrier();  // every wave is done reading Vs
-    if (has_next) {
-      const int jl = (j_next >= 0 && j_next < n_k) ? j_next : 0;
-      issue_v_tile<D, BLK>(Vs, vrs, jl, n_pad, w, lane);
-    }
-    j_cur = j_next;
+    // drain: P V of the last sub-tile S-1 (odd, so its probabilities are pb[1])
+    mfma_pair<D, BLK, false, true>(ka, 0, qreg, sc[0], va, (uint32_t)(((S - 1) % R) * C::SUB),
+                                   pb[1], oacc);
   }
 
   // ---- epilogue: O = O^T / l, lse -----------------------------------------
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = add_partner(l_run);
   const bool row_ok = (qrow < N) && (l_tot > 0.f);
   const float inv = row_ok ? 1.0f / l_tot : 0.f;
   __bf16* orow = O + head + (size_t)qrow * D;
@@ -277,7 +491,7 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     for (int qd = 0; qd < 4; ++qd) {
       f32x4_t v;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) v[t] = oacc[db][qd * 4 + t] * inv;
+      for (int u = 0; u < 4; ++u) v[u] = oacc[db][qd * 4 + u] * inv;
       const int d0 = db * 32 + qd * 8 + g * 4;
       *reinterpret_cast<bf16x4_t*>(orow + d0) = __builtin_convertvector(v, bf16x4_t);
     }
@@ -286,8 +500,11 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   }
 }
 
-// V [BH][n_pad][D] -> V^T [BH][D][n_pad] with the 16-key position permutation.
-// One workgroup transposes 64 keys x D of one head through LDS.
+// V [BH][n_pad][D] -> V^T in the LDS image of its 32-key sub-tiles: sub-tile y
+// of a head is SUB contiguous bytes, 16-byte chunk p of it holds d = 4*(p/16) +
+// (p/4)%4 and key positions 8c..8c+7 with c = (p%4) ^ ((p/16)%4); position q
+// of a 32-key sub-tile holds key (q & ~15) | perm16(q & 15).  One workgroup
+// transposes 64 keys (two sub-tiles) x D of one head through LDS.
 template <int D>
 __global__ void __launch_bounds__(256)
     transpose_v_kernel(const __bf16* __restrict__ V, __bf16* __restrict__ Vt, int n_pad) {
@@ -297,8 +514,7 @@ __global__ void __launch_bounds__(256)
   const int bh = blockIdx.y;
   const int n0 = blockIdx.x * TK;
   const __bf16* src = V + (size_t)bh * n_pad * D + (size_t)n0 * D;
-  __bf16* dst = Vt + (size_t)bh * D * n_pad + n0;
-  // load: TK rows of D bf16, 8 bf16 per thread-step
+  __bf16* dst = Vt + (size_t)bh * n_pad * D + (size_t)n0 * D;
   for (int c = threadIdx.x; c < TK * D / 8; c += 256) {
     const int row = c / (D / 8);
     const int col = (c % (D / 8)) * 8;
@@ -307,18 +523,21 @@ __global__ void __launch_bounds__(256)
     for (int t = 0; t < 8; ++t) tile[row * LD + col + t] = v[t];
   }
   __syncthreads();
-  // store: D rows of TK positions, 8 positions per thread-step
-  for (int c = threadIdx.x; c < D * TK / 8; c += 256) {
-    const int d = c / (TK / 8);
-    const int p0 = (c % (TK / 8)) * 8;
+  // output chunk q: sub-tile q / (4D), chunk p = q % (4D) of it
+  for (int q = threadIdx.x; q < TK * D / 8; q += 256) {
+    const int y = q / (4 * D);
+    const int p = q % (4 * D);
+    const int line = p >> 4;
+    const int d = line * 4 + ((p >> 2) & 3);
+    const int c = (p & 3) ^ (line & 3);
     bf16x8_t v;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      const int p = p0 + t;
-      const int key = (p & ~15) | perm16(p & 15);
+      const int pos = c * 8 + t;
+      const int key = y * 32 + ((pos & ~15) | perm16(pos & 15));
       v[t] = tile[key * LD + d];
     }
-    *reinterpret_cast<bf16x8_t*>(dst + (size_t)d * n_pad + p0) = v;
+    *reinterpret_cast<bf16x8_t*>(dst + (size_t)q * 8) = v;
   }
 }
 
@@ -363,7 +582,7 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, const void* q, const void* k, 
 }
 
 size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d) {
-  return (size_t)B * H * n_pad * d * 2;  // transposed V
+  return (size_t)B * H * n_pad * d * 2;  // V^T in sub-tile LDS images
 }
 
 }  // namespace losa

@@ -97,6 +97,8 @@ def test_select_capacity_is_checked_against_worst_case(L):
     (dict(q=None), 1), (dict(rp=None), 1), (dict(o=None), 1), (dict(ci=None), 1),
     (dict(cl=-1), 2), (dict(B=-1), 2), (dict(q=MIS), 4), (dict(o=MIS), 4), (dict(ws=MIS), 4),
     (dict(d=80), 5), (dict(bq=64, bk=128), 5), (dict(ws=None), 1), (dict(wsb=1), 6),
+    # more than 4096 key blocks per head: beyond the per-row LDS flags (both dtypes)
+    (dict(N=4097 * 128, d=64), 5), (dict(N=4097 * 128, d=64, dtype=0), 5),
 ])
 def test_fwd_validation(L, kw, code):
     assert _fwd(L, **kw) == code

@@ -284,6 +284,41 @@ def test_fwd_edge_case_csr(L):
     assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
 
 
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "f32-d128-blk128"])
+def test_fwd_repeated_ids_count_once(L, key):
+    # K(q) of Eq. (4) is a set: an id listed twice (or more) must weigh its
+    # keys once, exactly as the deduplicated row
+    w = SMALL[key]
+    q, k, v = W.make_inputs(w, device="cuda")
+    n_q = n_k = w.n_blocks
+    R = w.B * w.H * n_q
+    rng = np.random.default_rng(1234)
+    rows, clean = [], []
+    for r in range(R):
+        base = rng.choice(n_k, size=int(rng.integers(1, n_k + 1)), replace=False)
+        reps = rng.choice(base, size=int(rng.integers(1, 2 * n_k)), replace=True)
+        seg = np.concatenate([base, reps, [-3, n_k]])
+        rng.shuffle(seg)
+        rows.append(seg)
+        clean.append(np.sort(base))
+    rp = np.concatenate([[0], np.cumsum([len(x) for x in rows])]).astype(np.int64)
+    ci = np.concatenate(rows).astype(np.int64)
+    rp_c = np.concatenate([[0], np.cumsum([len(x) for x in clean])]).astype(np.int64)
+    ci_c = np.concatenate(clean).astype(np.int64)
+    say(f"repeated ids {key}: {R} rows, {ci.size} entries, {ci_c.size} distinct")
+    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block,
+                                    torch.from_numpy(rp.astype(np.int32)).cuda(),
+                                    torch.from_numpy(ci.astype(np.int32)).cuda(), want_lse=True)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+                                      rp_c, ci_c)
+    tmax, tmean = out_tol(w)
+    mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
+    assert mx <= tmax and mean <= tmean, (mx, mean)
+    valid = ~np.isneginf(l_ref)
+    assert np.abs(f64(lse)[valid] - l_ref[valid]).max() <= LSE_TOL
+
+
 def test_deterministic(L):
     w = SMALL["cog-bf16-d64-ragged"]
     q, k, v = W.make_inputs(w, device="cuda")
