@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-reference-mib", type=int, default=0,
+                    help="first run one plain device-to-device copy of this many MiB, a "
+                         "reference of known size for hardware byte counters")
     return ap.parse_args()
 
 
@@ -141,6 +144,14 @@ def main():
     ws_fwd = torch.empty(max(L.workspace_bytes(2, 1 if w.dtype == "bf16" else 0, w.B, w.H, N, d,
                                                C, C), 16), dtype=torch.uint8, device=dev)
     out = torch.empty_like(q0)
+    if args.copy_reference_mib > 0:
+        nbytes = args.copy_reference_mib << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     def step():

@@ -164,13 +164,32 @@ __device__ __forceinline__ void mfma_pair(const uint32_t* ka, uint32_t kimm, con
   }
 }
 
+// Probabilities of one 32-key sub-tile for this lane's 16 scores against the
+// running max m_run (log2 units): bf16-packed into pcur; returns their fp32 sum.
+__device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_log2, float m_run,
+                                             bf16x8_t* pcur) {
+  float ls0 = 0.f, ls1 = 0.f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    f32x8_t p;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = fast_exp2(__builtin_fmaf(cur[8 * h + e], scale_log2, -m_run));
+      if (e & 1) ls1 += p[e]; else ls0 += p[e];
+    }
+    pcur[h] = __builtin_convertvector(p, bf16x8_t);
+  }
+  return ls0 + ls1;
+}
+
 // One pipelined sub-iteration, issued in a fixed order: NM = KS + 2*DB MFMAs
 // alternate between S^T(next) = K Q^T (a KS-long dependent chain) and
 // O^T += V^T P^T(prev) (2 k-steps x DB independent chains); each MFMA's LDS
-// operand is read NPRE MFMAs ahead from a small register ring, and after each
-// MFMA the VALU exponentiates 16/NM elements of the current scores (fp32 sum
-// and bf16 pack).  sched_group_barrier fixes this order, so the LDS latency
-// and the softmax both hide behind the matrix cores.
+// operand is read NPRE MFMAs ahead from a small register ring.  The softmax
+// of the current sub-tile runs in their shadow: under each of the first NM/2
+// MFMAs two scores are scaled (v_fma) and exponentiated (v_exp, a
+// transcendental), under each of the last NM/2 the bf16 packs and the fp32
+// row-sum adds.  sched_group_barrier fixes this order.
 template <int D, int BLK, int NPRE>
 __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm,
                                                const bf16x8_t* qreg, f32x16_t& snext,
@@ -179,8 +198,8 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
                                                float scale_log2, float m_run, bf16x8_t* pcur) {
   using C = FwdCfg<D, BLK>;
   constexpr int NM = C::KS + 2 * C::DB;
-  constexpr int EPS = 16 / NM;  // softmax elements per MFMA
-  static_assert(EPS * NM == 16, "softmax elements split evenly over the MFMAs");
+  static_assert(NM == 16 || NM == 8, "softmax split written for 8 or 16 MFMAs");
+  constexpr int EPM = 32 / NM;  // exponentials per MFMA in the first half
   auto read_op = [&](int i) -> bf16x8_t {
     if ((i & 1) == 0) return lds_read16(ka[i >> 1] + kimm);
     const int st = (i >> 1) / C::DB, db = (i >> 1) % C::DB;
@@ -190,7 +209,7 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
 #pragma unroll
   for (int i = 0; i < NPRE; ++i) ring[i] = read_op(i);
   float ls0 = 0.f, ls1 = 0.f;
-  f32x8_t p;
+  f32x8_t p[2];
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     const bf16x8_t a = ring[i % NPRE];
@@ -203,23 +222,33 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pprev[st], o[db], 0, 0, 0);
     }
     if (i + NPRE < NM) ring[i % NPRE] = read_op(i + NPRE);
+    if (i < NM / 2) {
 #pragma unroll
-    for (int u = 0; u < EPS; ++u) {
-      const int e = i * EPS + u;
-      const float pe = fast_exp2(__builtin_fmaf(cur[e], scale_log2, -m_run));
-      p[e & 7] = pe;
-      if (e & 1) ls1 += pe; else ls0 += pe;
-      if ((e & 7) == 7) pcur[e >> 3] = __builtin_convertvector(p, bf16x8_t);
+      for (int u = 0; u < EPM; ++u) {
+        const int e = i * EPM + u;
+        p[e >> 3][e & 7] = fast_exp2(__builtin_fmaf(cur[e], scale_log2, -m_run));
+      }
     }
   }
-  // fixed issue order: the NPRE lead reads, then per MFMA the next read and
-  // the softmax work of its elements
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    pcur[h] = __builtin_convertvector(p[h], bf16x8_t);
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) { ls0 += p[h][e]; ls1 += p[h][e + 1]; }
+  }
+  // fixed issue order: the NPRE lead reads; then per MFMA the next read and
+  // either EPM (fma, exp) pairs or its share of the packs and sums
   __builtin_amdgcn_sched_group_barrier(0x100, NPRE, 0);
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     if (i + NPRE < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 3 * EPS, 0);
+    if (i < NM / 2) {
+      __builtin_amdgcn_sched_group_barrier(0x002, EPM, 0);  // v_fma
+      __builtin_amdgcn_sched_group_barrier(0x400, EPM, 0);  // v_exp
+    } else {
+      __builtin_amdgcn_sched_group_barrier(0x002, 48 / NM, 0);  // v_cvt_pk / v_add
+    }
   }
   // pin the softmax results here: otherwise the compiler sinks the exp2 work
   // next to its consumers in the following sub-iteration, out of the shadow
@@ -246,10 +275,11 @@ __device__ __forceinline__ void mask_sub(f32x16_t& s, int part, int kvalid, int 
   }
 }
 
-// Lazy rescale threshold (log2 units): the running max used for exp2 is only
-// raised when a sub-tile's max exceeds it by more than this, so probabilities
-// stay <= 2^8 and the O rescale is skipped on most sub-tiles.
-constexpr float kRescaleThreshold = 8.0f;
+// Bound on one lane's sum of 16 probabilities of a sub-tile (so on each of
+// them) before the running max must be raised.  The running max then trails
+// the true one by at most log2 of it; l and O stay far from fp32 overflow
+// (at most 2^20 per key over at most 2^19 keys).
+constexpr float kSumBound = 1048576.0f;
 
 template <int D, int BLK>
 __global__ void __launch_bounds__(BLK * 2)
@@ -400,8 +430,8 @@ __global__ void __launch_bounds__(BLK * 2)
     // Sub-iteration s = R*u + H (H static).  On entry the raw scores of s are
     // in sc[H & 1] and the probabilities of s-1 in pb[(H + 1) & 1].  The
     // matrix cores compute the scores of s+1 (K slot (H+1) % R) alternating
-    // with P V of s-1 (V^T slot (H-1) % R); the VALU exponentiates s.  The
-    // lazy O rescale decided for s is applied after P V(s-1), before P V(s).
+    // with P V of s-1 (V^T slot (H-1) % R); the VALU exponentiates s.  A
+    // rescale found necessary for s is applied after P V(s-1), before P V(s).
     // The scores computed for sub-tile S (after the last) are never used; the
     // first P V multiplies zero probabilities with the zeroed slot.
     auto sub_iter = [&](auto hh, int u) {
@@ -428,23 +458,26 @@ __global__ void __launch_bounds__(BLK * 2)
       // ragged last key block: mask the keys >= N of this sub-tile
       const int kvb = N - jc[H / NS] * BLK;
       if (kvb < (H % NS + 1) * 32) mask_sub(cur, H % NS, kvb, g);
-      // lazy rescale decision for s (wave-uniform)
-      const float ms = sub_max(cur) * scale_log2;
-      const bool resc = __ballot(ms > m_run + kRescaleThreshold) != 0;
-      float alpha = 1.f;
-      if (resc) {
+      float ls = pipeline_step<D, BLK, 4>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
+                                          ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc,
+                                          cur, scale_log2, m_run, pb[H & 1]);
+      // The probabilities of s were taken against the running max without
+      // looking at this sub-tile's scores.  If a lane's sum exceeds the bound
+      // (or is inf: the first sub-tile, or a jump of the max), raise the max
+      // to this sub-tile's and redo them; O^T, which now holds P V up to s-1,
+      // and l move to the new reference.  Every probability that reaches P V
+      // is therefore at most kSumBound.
+      if (__ballot(!(ls <= kSumBound)) != 0) {
+        const float ms = sub_max(cur) * scale_log2;
         const float m_new = fmaxf(m_run, ms);
-        alpha = fast_exp2(m_run - m_new);
+        const float alpha = fast_exp2(m_run - m_new);
         m_run = m_new;
         l_run *= alpha;
-      }
-      l_run += pipeline_step<D, BLK, 4>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
-                                        ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc, cur,
-                                        scale_log2, m_run, pb[H & 1]);
-      if (resc) {
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) oacc[db] *= alpha;
+        ls = softmax_sub(cur, scale_log2, m_run, pb[H & 1]);
       }
+      l_run += ls;
     };
 
     using I0 = std::integral_constant<int, 0>;
