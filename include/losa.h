@@ -123,9 +123,10 @@ losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block
  *             padding rows are 0.
  * lse         out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp over
  *             K(q) of the scaled scores; -inf for empty or padding rows.
- * workspace   >= losa_workspace_bytes(2, ...) bytes (bf16: a transposed copy
- *             of V in the kernel's tile layout, B*H*N_pad*d*2 bytes, rewritten
- *             by every call; f32: none).
+ * workspace   >= losa_workspace_bytes(2, ...) bytes, rewritten by every call
+ *             (bf16: a transposed copy of V in the kernel's tile layout,
+ *             B*H*N_pad*d*2 bytes rounded up to 256, then the rows' dispatch
+ *             order, 4*B*H*n_q bytes; f32: none).
  * Arithmetic (bf16): Q K^T and P V on bf16 matrix cores with fp32
  * accumulation, softmax in fp32, P rounded to bf16 for the P V product, O
  * rounded to bf16 once at the end.  f32: fp32 throughout.

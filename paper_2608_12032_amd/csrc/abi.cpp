@@ -172,7 +172,7 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
                 losa::kSparseFwdMaxNk);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (dtype == LOSA_DTYPE_BF16) {
-    const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d);
+    const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q);
     if (!workspace) return fail(LOSA_ERR_NULL_POINTER, "bf16 needs a workspace of %zu bytes", need);
     if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
     if (workspace_bytes < need)
@@ -197,7 +197,7 @@ size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, in
     case 1:
       return losa::select_workspace_bytes((int)s.rows, s.n_k);
     case 2:
-      return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d) : 0;
+      return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) : 0;
     default:
       return 0;
   }

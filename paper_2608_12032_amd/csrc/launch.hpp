@@ -38,7 +38,7 @@ hipError_t launch_sparse_fwd_f32(int d, int blk, const void* q, const void* k, c
                                  int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
                                  void* o, float* lse, hipStream_t stream);
-size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d);
+size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d, int n_q);
 
 // Largest n_k (key blocks per head) the sparse forward kernels accept: each
 // workgroup keeps one flag per key block of its row in LDS.

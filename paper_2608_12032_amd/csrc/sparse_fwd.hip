@@ -287,8 +287,9 @@ __global__ void __launch_bounds__(BLK * 2)
     sparse_fwd_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                            const __bf16* __restrict__ Vt, const int32_t* __restrict__ row_ptr,
                            const int32_t* __restrict__ col_idx, int64_t col_len,
-                           __bf16* __restrict__ O, float* __restrict__ lse, int rows_total,
-                           int n_q, int n_k, int N, int n_pad, float scale_log2) {
+                           __bf16* __restrict__ O, float* __restrict__ lse,
+                           const int* __restrict__ order, int n_q, int n_k, int N, int n_pad,
+                           float scale_log2) {
   using C = FwdCfg<D, BLK>;
   constexpr int NS = C::NS;
   constexpr int R = C::R;
@@ -303,7 +304,7 @@ __global__ void __launch_bounds__(BLK * 2)
   const int l32 = lane & 31;
   const int g = lane >> 5;
 
-  const int r = xcd_remap(blockIdx.x, rows_total);
+  const int r = order[blockIdx.x];
   const int bh = r / n_q;
   const int qb = r - bh * n_q;
   const size_t head = (size_t)bh * n_pad * D;
@@ -533,6 +534,66 @@ __global__ void __launch_bounds__(BLK * 2)
   }
 }
 
+// Dispatch order of the CSR rows.  Workgroup ids are dealt round-robin over
+// the 8 XCDs, so id 8*k + x runs on XCD x as that XCD's k-th row.  XCD x gets
+// a contiguous range of rows (neighbouring query blocks of one head retain
+// mostly the same key blocks and so share its L2), ordered by decreasing
+// length: the longest rows start first and the last to finish are short ones
+// (longest-processing-time-first list scheduling).  One workgroup per XCD
+// counting-sorts its range by length; rows of equal length land in any order,
+// which changes only the schedule, never a result.
+constexpr int kOrderThreads = 1024;
+
+__global__ void __launch_bounds__(kOrderThreads)
+    order_rows_kernel(const int32_t* __restrict__ row_ptr, int64_t col_len, int rows, int n_k,
+                      int* __restrict__ order) {
+  constexpr int NT = kOrderThreads;
+  __shared__ int bins[kSparseFwdMaxNk + 1];  // bin n_k - len
+  __shared__ int part[NT];
+  const int tid = threadIdx.x;
+  const int x = blockIdx.x;
+  auto count_of = [&](int y) { return rows > y ? (rows - y + 7) / 8 : 0; };
+  const int cnt = count_of(x);
+  int start = 0;
+  for (int y = 0; y < x; ++y) start += count_of(y);
+  auto len_of = [&](int r) {
+    int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
+    return (int)(e1 - e0 < n_k ? e1 - e0 : n_k);
+  };
+  const int nb = n_k + 1;
+  for (int b = tid; b < nb; b += NT) bins[b] = 0;
+  __syncthreads();
+  for (int k = tid; k < cnt; k += NT) atomicAdd(&bins[n_k - len_of(start + k)], 1);
+  __syncthreads();
+  // exclusive scan of the bins: per-thread chunks, then a scan of the chunk sums
+  const int per = (nb + NT - 1) / NT;
+  const int lo = min(nb, tid * per), hi = min(nb, lo + per);
+  int sum = 0;
+  for (int b = lo; b < hi; ++b) sum += bins[b];
+  part[tid] = sum;
+  __syncthreads();
+  for (int off = 1; off < NT; off <<= 1) {
+    const int add = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += add;
+    __syncthreads();
+  }
+  int run = tid > 0 ? part[tid - 1] : 0;
+  for (int b = lo; b < hi; ++b) {
+    const int c = bins[b];
+    bins[b] = run;
+    run += c;
+  }
+  __syncthreads();
+  for (int k = tid; k < cnt; k += NT) {
+    const int r = start + k;
+    const int pos = atomicAdd(&bins[n_k - len_of(r)], 1);
+    order[pos * 8 + x] = r;
+  }
+}
+
 // V [BH][n_pad][D] -> V^T in the LDS image of its 32-key sub-tiles: sub-tile y
 // of a head is SUB contiguous bytes, 16-byte chunk p of it holds d = 4*(p/16) +
 // (p/4)%4 and key positions 8c..8c+7 with c = (p%4) ^ ((p/16)%4); position q
@@ -574,21 +635,29 @@ __global__ void __launch_bounds__(256)
   }
 }
 
+// Workspace layout: V^T (B*H*n_pad*D bf16), then the dispatch order (one int
+// per row) at the next 256-byte boundary.
+size_t vt_bytes(int BH, int n_pad, int d) { return ((size_t)BH * n_pad * d * 2 + 255) / 256 * 256; }
+
 template <int D, int BLK>
 hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H, int N, int n_pad,
                       float scale, const int32_t* row_ptr, const int32_t* col_idx,
-                      int64_t col_len, void* o, float* lse, void* vt, hipStream_t stream) {
+                      int64_t col_len, void* o, float* lse, void* workspace, hipStream_t stream) {
   const int BH = B * H;
   const int n_q = n_pad / BLK;
   const int n_k = n_pad / BLK;
+  const int rows = BH * n_q;
+  __bf16* vt = static_cast<__bf16*>(workspace);
+  int* order = reinterpret_cast<int*>(static_cast<char*>(workspace) + vt_bytes(BH, n_pad, D));
+  hipLaunchKernelGGL(order_rows_kernel, dim3(8), dim3(kOrderThreads), 0, stream, row_ptr, col_len,
+                     rows, n_k, order);
   dim3 tgrid(n_pad / 64, BH);
   hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
-                     static_cast<const __bf16*>(v), static_cast<__bf16*>(vt), n_pad);
-  const int rows = BH * n_q;
+                     static_cast<const __bf16*>(v), vt, n_pad);
   hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK>), dim3(rows), dim3(FwdCfg<D, BLK>::NT), 0,
                      stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(vt), row_ptr, col_idx, col_len,
-                     static_cast<__bf16*>(o), lse, rows, n_q, n_k, N, n_pad, scale * kLog2e);
+                     static_cast<__bf16*>(o), lse, order, n_q, n_k, N, n_pad, scale * kLog2e);
   return hipGetLastError();
 }
 
@@ -614,8 +683,9 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, const void* q, const void* k, 
   return hipErrorInvalidValue;
 }
 
-size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d) {
-  return (size_t)B * H * n_pad * d * 2;  // V^T in sub-tile LDS images
+size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d, int n_q) {
+  // V^T in sub-tile LDS images, then the rows' dispatch order
+  return vt_bytes(B * H, n_pad, d) + (size_t)B * H * n_q * sizeof(int);
 }
 
 }  // namespace losa

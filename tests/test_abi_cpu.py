@@ -107,7 +107,7 @@ def test_fwd_validation(L, kw, code):
 def test_workspace_sizes(L):
     B, H, N, d = 1, 12, 32760, 128
     assert L.workspace_bytes(0, 1, B, H, N, d, 128, 128) == 0
-    assert L.workspace_bytes(2, 1, B, H, N, d, 128, 128) == B * H * 32768 * d * 2
+    assert L.workspace_bytes(2, 1, B, H, N, d, 128, 128) == B * H * 32768 * d * 2 + B * H * 256 * 4
     assert L.workspace_bytes(2, 0, B, H, N, d, 128, 128) == 0
     rows, n_k = 12 * 256, 256
     assert L.workspace_bytes(1, 0, B, H, N, 1, 128, 128) == ((rows * 4 + 255) // 256) * 256 + rows * n_k

@@ -319,6 +319,30 @@ def test_fwd_repeated_ids_count_once(L, key):
     assert np.abs(f64(lse)[valid] - l_ref[valid]).max() <= LSE_TOL
 
 
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "cog-bf16-d64-ragged"])
+def test_fwd_writes_every_row_once(L, key):
+    # the forward dispatches rows in a computed order (per-XCD, longest
+    # first): every row of O and lse must be written, with the row count not
+    # a multiple of 8 and rows of equal length; poison the outputs first
+    w = SMALL[key]
+    q, k, v = W.make_inputs(w, device="cuda")
+    R = w.B * w.H * w.n_blocks
+    say(f"every row {key}: {R} rows")
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block)
+    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, w.tau)
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((w.B, w.H, w.N_pad), float("nan"), dtype=torch.float32, device=q.device)
+    L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci, want_lse=True, out=o, lse=lse)
+    torch.cuda.synchronize()
+    assert not torch.isnan(o).any().item()
+    assert not torch.isnan(lse).any().item()
+    o_ref, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+                                  rp.cpu().numpy().astype(np.int64),
+                                  ci[:L.nnz(rp)].cpu().numpy().astype(np.int64))
+    mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
+    assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
+
+
 def test_deterministic(L):
     w = SMALL["cog-bf16-d64-ragged"]
     q, k, v = W.make_inputs(w, device="cuda")
