@@ -34,10 +34,14 @@
 // reads K sub-tile s+1 (scores of the next sub-tile) and V^T sub-tile s-1
 // (P V of the previous one); after the barrier that opens it, the slots that
 // sub-iteration s-1 finished with are refilled with K sub-tile s+kRing and V^T
-// sub-tile s+kRing-2, both needed kRing-1 sub-iterations later.  Inside a
-// sub-iteration the matrix cores alternate the next scores with P V of the
-// previous sub-tile while the VALU exponentiates the current one; the
-// instruction interleave is fixed with sched_group_barrier.
+// sub-tile s+kRing-2, both needed kRing-1 sub-iterations later.  Every
+// sub-iteration issues the same number of loads (past the end of the stream
+// they fetch the last block again), so one fixed vmcnt wait before each
+// barrier is exact.  Inside a sub-iteration the matrix cores alternate the
+// next scores with P V of the previous sub-tile while the VALU exponentiates
+// the current one, and the loads leave one at a time between the MFMAs
+// rather than in a burst; the instruction interleave is fixed with
+// sched_group_barrier.
 //
 // LDS images.  A K sub-tile is 32 rows of D bf16, row-major, 16-byte chunks
 // XOR-swizzled by 256-byte line; V^T is kept in global memory already in the
@@ -99,18 +103,34 @@ __device__ __forceinline__ int kswz(int row, int c) {
   return c ^ ((row / C::KRPL) % C::KCPR);
 }
 
-// NL consecutive 1 KiB direct loads of one wave into LDS at dst: load u moves
-// 16 bytes per lane from offs[u] (or voff + 1024*u when offs is null) plus the
-// wave-uniform sbase.
-template <int NL>
-__device__ __forceinline__ void wave_loads(char* dst, __amdgpu_buffer_rsrc_t rs,
-                                           const uint32_t* offs, uint32_t voff, uint32_t sbase) {
-#pragma unroll
-  for (int u = 0; u < NL; ++u)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        rs, (__attribute__((address_space(3))) void*)(dst + u * 1024), 16,
-        offs ? offs[u] : voff + u * 1024, sbase, 0, 0);
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base + bytes) in scalar registers (the
+// fields make_rsrc fills): an offset outside the range reads zero.
+__device__ __forceinline__ i32x4_t rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
 }
+
+// One wave-wide 16-byte-per-lane buffer load straight into LDS: lane L's 16
+// bytes at rs + voff + soff land at LDS byte lds + 16 L (lds wave-uniform).
+// Written as inline assembly so that the compiler does not hold the LDS reads
+// that follow it until it completes: the kernel guarantees they never touch
+// the slot it writes, and waits for it explicitly (vmcnt) before the barrier
+// that publishes the slot.  M0 carries the LDS address; the compiler emits
+// no M0 use of its own in these kernels, so nothing it keeps there is lost.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // M0 is reserved: see above
+__device__ __forceinline__ void dma16(uint32_t lds, const i32x4_t& rs, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rs), "s"(soff) : "m0");
+}
+#pragma clang diagnostic pop
 
 // max / sum of a value and the one held by lane ^ 32 (v_permlane32_swap gives
 // each lane the pair {own, partner} in some order; max and + do not care).
@@ -173,11 +193,10 @@ __device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_lo
   for (int h = 0; h < 2; ++h) {
     f32x8_t p;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = fast_exp2(__builtin_fmaf(cur[8 * h + e], scale_log2, -m_run));
-      if (e & 1) ls1 += p[e]; else ls0 += p[e];
-    }
+    for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(cur[8 * h + e], scale_log2, -m_run));
     pcur[h] = __builtin_convertvector(p, bf16x8_t);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { if (e & 1) ls1 += p[e]; else ls0 += p[e]; }
   }
   return ls0 + ls1;
 }
@@ -188,23 +207,29 @@ __device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_lo
 // operand is read NPRE MFMAs ahead from a small register ring.  The softmax
 // of the current sub-tile runs in their shadow: under each of the first NM/2
 // MFMAs two scores are scaled (v_fma) and exponentiated (v_exp, a
-// transcendental), under each of the last NM/2 the bf16 packs and the fp32
-// row-sum adds.  sched_group_barrier fixes this order.
-template <int D, int BLK, int NPRE>
+// transcendental), under each of the last NM/2 the bf16 packs and the row
+// sums.  The NL global->LDS loads of this sub-iteration (issue(t), t < NL)
+// are spread evenly over the MFMAs instead of leaving in one burst.
+// sched_group_barrier fixes this order.
+template <int D, int BLK, int NPRE, int NL, typename Issue>
 __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm,
                                                const bf16x8_t* qreg, f32x16_t& snext,
                                                const uint32_t* va, uint32_t vimm,
                                                const bf16x8_t* pprev, f32x16_t* o, f32x16_t& cur,
-                                               float scale_log2, float m_run, bf16x8_t* pcur) {
+                                               float scale_log2, float m_run, bf16x8_t* pcur,
+                                               Issue&& issue) {
   using C = FwdCfg<D, BLK>;
   constexpr int NM = C::KS + 2 * C::DB;
   static_assert(NM == 16 || NM == 8, "softmax split written for 8 or 16 MFMAs");
+  static_assert(NL <= NM, "at most one load per MFMA");
   constexpr int EPM = 32 / NM;  // exponentials per MFMA in the first half
   auto read_op = [&](int i) -> bf16x8_t {
     if ((i & 1) == 0) return lds_read16(ka[i >> 1] + kimm);
     const int st = (i >> 1) / C::DB, db = (i >> 1) % C::DB;
     return lds_read16(va[st] + vimm + db * C::VDB);
   };
+  // load t is issued right after MFMA t * NM / NL
+  auto has_load = [&](int i) { return (i * NL) % NM == 0; };
   bf16x8_t ring[NPRE];
 #pragma unroll
   for (int i = 0; i < NPRE; ++i) ring[i] = read_op(i);
@@ -222,6 +247,7 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pprev[st], o[db], 0, 0, 0);
     }
     if (i + NPRE < NM) ring[i % NPRE] = read_op(i + NPRE);
+    if (has_load(i)) issue((i * NL) / NM);
     if (i < NM / 2) {
 #pragma unroll
       for (int u = 0; u < EPM; ++u) {
@@ -236,18 +262,21 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
 #pragma unroll
     for (int e = 0; e < 8; e += 2) { ls0 += p[h][e]; ls1 += p[h][e + 1]; }
   }
-  // fixed issue order: the NPRE lead reads; then per MFMA the next read and
-  // either EPM (fma, exp) pairs or its share of the packs and sums
+  // fixed issue order: the NPRE lead reads; then per MFMA the next read, its
+  // load if it has one, and either EPM (fma, exp) pairs or its share of the
+  // 8 packs and 16 sums of the second half
+  constexpr int TAIL = 24;
   __builtin_amdgcn_sched_group_barrier(0x100, NPRE, 0);
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     if (i + NPRE < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    if (has_load(i)) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
     if (i < NM / 2) {
       __builtin_amdgcn_sched_group_barrier(0x002, EPM, 0);  // v_fma
       __builtin_amdgcn_sched_group_barrier(0x400, EPM, 0);  // v_exp
     } else {
-      __builtin_amdgcn_sched_group_barrier(0x002, 48 / NM, 0);  // v_cvt_pk / v_add
+      __builtin_amdgcn_sched_group_barrier(0x002, 2 * TAIL / NM, 0);  // v_cvt_pk / sums
     }
   }
   // pin the softmax results here: otherwise the compiler sinks the exp2 work
@@ -309,8 +338,8 @@ __global__ void __launch_bounds__(BLK * 2)
   const int qb = r - bh * n_q;
   const size_t head = (size_t)bh * n_pad * D;
   const uint32_t head_bytes = (uint32_t)((size_t)n_pad * D * 2);
-  const __amdgpu_buffer_rsrc_t krs = make_rsrc(K + head, head_bytes);
-  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(Vt + head, head_bytes);
+  const i32x4_t krs = rsrc_words(K + head, head_bytes);
+  const i32x4_t vrs = rsrc_words(Vt + head, head_bytes);
 
   // ---- the row's distinct valid key blocks, ascending ---------------------
   // (flags and per-wave counts live in the rings, unused until the first load)
@@ -384,12 +413,16 @@ __global__ void __launch_bounds__(BLK * 2)
 
   // key sub-tile (block j, part) -> K slot x / V^T slot x
   auto load_k = [&](int x, int j, int part) {
-    wave_loads<C::LPW>(smem + x * C::SUB + w * C::LPW * 1024, krs, koffs, 0,
-                       (uint32_t)((j * BLK + part * 32) * C::KROW));
+#pragma unroll
+    for (int u = 0; u < C::LPW; ++u)
+      dma16(lds0 + x * C::SUB + (w * C::LPW + u) * 1024, krs, koffs[u],
+            (uint32_t)((j * BLK + part * 32) * C::KROW));
   };
   auto load_v = [&](int x, int j, int part) {
-    wave_loads<C::LPW>(smem + C::RING + x * C::SUB + w * C::LPW * 1024, vrs, nullptr, voff0,
-                       (uint32_t)((j * NS + part) * C::SUB));
+#pragma unroll
+    for (int u = 0; u < C::LPW; ++u)
+      dma16(lds0 + C::RING + x * C::SUB + (w * C::LPW + u) * 1024, vrs, voff0 + u * 1024,
+            (uint32_t)((j * NS + part) * C::SUB));
   };
   // list entry x as a scalar, clamped into the list
   auto block_at = [&](int x) -> int {
@@ -446,22 +479,29 @@ __global__ void __launch_bounds__(BLK * 2)
       launder(va[1]);
       // K sub-tile s+1 and V^T sub-tile s-1 (loaded R-1 sub-iterations ago)
       // have landed for every wave, and every wave is done with sub-iteration
-      // s-1; loads of later passes may still be in flight unless the stream
-      // ends within them (then some were not issued and the count is off)
-      if (s - 1 + R < S) wait_vm_barrier<(R - 2) * 2 * C::LPW>(); else wait_vm_barrier<0>();
+      // s-1.  Every sub-iteration issues the same loads (past the end of the
+      // stream they fetch the last block again), so the count is exact.
+      wait_vm_barrier<(R - 2) * 2 * C::LPW>();
+      constexpr int HV = H + R - 2;  // pass-relative index of sub-tile s+R-2
+      const int jk = jn[H / NS];
+      const int jv = (HV < R) ? jc[(HV < R ? HV : 0) / NS] : jn[(HV < R ? 0 : HV - R) / NS];
       // refill: K slot H <- K sub-tile s+R, V^T slot (H+R-2) % R <- sub-tile s+R-2
-      if (s + R < S) load_k(H, jn[H / NS], H % NS);
-      if (s + R - 2 < S) {
-        constexpr int HV = H + R - 2;  // pass-relative index of sub-tile s+R-2
-        const int jv = (HV < R) ? jc[(HV < R ? HV : 0) / NS] : jn[(HV < R ? 0 : HV - R) / NS];
-        load_v(HV % R, jv, HV % NS);
-      }
+      auto issue = [&](int t) {
+        if (t < C::LPW) {
+          dma16(lds0 + H * C::SUB + (w * C::LPW + t) * 1024, krs, koffs[t],
+                (uint32_t)((jk * BLK + (H % NS) * 32) * C::KROW));
+        } else {
+          const int u = t - C::LPW;
+          dma16(lds0 + C::RING + (HV % R) * C::SUB + (w * C::LPW + u) * 1024, vrs, voff0 + u * 1024,
+                (uint32_t)((jv * NS + HV % NS) * C::SUB));
+        }
+      };
       // ragged last key block: mask the keys >= N of this sub-tile
       const int kvb = N - jc[H / NS] * BLK;
       if (kvb < (H % NS + 1) * 32) mask_sub(cur, H % NS, kvb, g);
-      float ls = pipeline_step<D, BLK, 4>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
+      float ls = pipeline_step<D, BLK, 4, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
                                           ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc,
-                                          cur, scale_log2, m_run, pb[H & 1]);
+                                          cur, scale_log2, m_run, pb[H & 1], issue);
       // The probabilities of s were taken against the running max without
       // looking at this sub-tile's scores.  If a lane's sum exceeds the bound
       // (or is inf: the first sub-tile, or a jump of the max), raise the max
@@ -509,6 +549,9 @@ __global__ void __launch_bounds__(BLK * 2)
         jn[x] = __builtin_amdgcn_readfirstlane(jf[x]);
       }
     }
+    // the last passes issued loads that nothing reads: let them land before
+    // the workgroup's LDS can be handed to another workgroup
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     // drain: P V of the last sub-tile S-1 (odd, so its probabilities are pb[1])
     mfma_pair<D, BLK, false, true>(ka, 0, qreg, sc[0], va, (uint32_t)(((S - 1) % R) * C::SUB),
                                    pb[1], oacc);
@@ -536,61 +579,43 @@ __global__ void __launch_bounds__(BLK * 2)
 
 // Dispatch order of the CSR rows.  Workgroup ids are dealt round-robin over
 // the 8 XCDs, so id 8*k + x runs on XCD x as that XCD's k-th row.  XCD x gets
-// a contiguous range of rows (neighbouring query blocks of one head retain
-// mostly the same key blocks and so share its L2), ordered by decreasing
-// length: the longest rows start first and the last to finish are short ones
-// (longest-processing-time-first list scheduling).  One workgroup per XCD
-// counting-sorts its range by length; rows of equal length land in any order,
-// which changes only the schedule, never a result.
-constexpr int kOrderThreads = 1024;
+// a contiguous range of rows, cut into chunks of kOrderChunk consecutive rows
+// (neighbouring query blocks of one head, which retain mostly the same key
+// blocks).  The chunks run in order, so the rows in flight on an XCD at any
+// time come from one or two chunks and share its L2; inside a chunk rows go
+// longest first (longest-processing-time-first list scheduling), so the tail
+// of the launch is made of short rows.  Ties keep the row order.  The order
+// changes only the schedule, never a result.
+constexpr int kOrderChunk = 128;
 
-__global__ void __launch_bounds__(kOrderThreads)
+// One workgroup per (chunk c = blockIdx.x, XCD x = blockIdx.y): the chunk's
+// row lengths go to LDS, then each thread ranks one row against them.
+__global__ void __launch_bounds__(kOrderChunk)
     order_rows_kernel(const int32_t* __restrict__ row_ptr, int64_t col_len, int rows, int n_k,
                       int* __restrict__ order) {
-  constexpr int NT = kOrderThreads;
-  __shared__ int bins[kSparseFwdMaxNk + 1];  // bin n_k - len
-  __shared__ int part[NT];
-  const int tid = threadIdx.x;
-  const int x = blockIdx.x;
+  __shared__ int len[kOrderChunk];
+  const int x = blockIdx.y;
+  const int c0 = blockIdx.x * kOrderChunk;
   auto count_of = [&](int y) { return rows > y ? (rows - y + 7) / 8 : 0; };
   const int cnt = count_of(x);
-  int start = 0;
+  if (c0 >= cnt) return;  // this XCD has fewer chunks (uniform per workgroup)
+  int start = 0;  // XCD x owns rows [start, start + cnt)
   for (int y = 0; y < x; ++y) start += count_of(y);
-  auto len_of = [&](int r) {
+  const int n = min(cnt - c0, kOrderChunk);
+  const int t = threadIdx.x;
+  if (t < n) {
+    const int r = start + c0 + t;
     int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
     e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
     e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
-    return (int)(e1 - e0 < n_k ? e1 - e0 : n_k);
-  };
-  const int nb = n_k + 1;
-  for (int b = tid; b < nb; b += NT) bins[b] = 0;
-  __syncthreads();
-  for (int k = tid; k < cnt; k += NT) atomicAdd(&bins[n_k - len_of(start + k)], 1);
-  __syncthreads();
-  // exclusive scan of the bins: per-thread chunks, then a scan of the chunk sums
-  const int per = (nb + NT - 1) / NT;
-  const int lo = min(nb, tid * per), hi = min(nb, lo + per);
-  int sum = 0;
-  for (int b = lo; b < hi; ++b) sum += bins[b];
-  part[tid] = sum;
-  __syncthreads();
-  for (int off = 1; off < NT; off <<= 1) {
-    const int add = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += add;
-    __syncthreads();
-  }
-  int run = tid > 0 ? part[tid - 1] : 0;
-  for (int b = lo; b < hi; ++b) {
-    const int c = bins[b];
-    bins[b] = run;
-    run += c;
+    len[t] = (int)(e1 - e0 < n_k ? e1 - e0 : n_k);
   }
   __syncthreads();
-  for (int k = tid; k < cnt; k += NT) {
-    const int r = start + k;
-    const int pos = atomicAdd(&bins[n_k - len_of(r)], 1);
-    order[pos * 8 + x] = r;
+  if (t < n) {
+    const int mine = len[t];
+    int rank = 0;  // rows of the chunk that go before this one
+    for (int y = 0; y < n; ++y) rank += (len[y] > mine) || (len[y] == mine && y < t);
+    order[(c0 + rank) * 8 + x] = start + c0 + t;
   }
 }
 
@@ -649,8 +674,9 @@ hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H,
   const int rows = BH * n_q;
   __bf16* vt = static_cast<__bf16*>(workspace);
   int* order = reinterpret_cast<int*>(static_cast<char*>(workspace) + vt_bytes(BH, n_pad, D));
-  hipLaunchKernelGGL(order_rows_kernel, dim3(8), dim3(kOrderThreads), 0, stream, row_ptr, col_len,
-                     rows, n_k, order);
+  const int per_xcd = (rows + 7) / 8;
+  hipLaunchKernelGGL(order_rows_kernel, dim3((per_xcd + kOrderChunk - 1) / kOrderChunk, 8),
+                     dim3(kOrderChunk), 0, stream, row_ptr, col_len, rows, n_k, order);
   dim3 tgrid(n_pad / 64, BH);
   hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
                      static_cast<const __bf16*>(v), vt, n_pad);
