@@ -50,6 +50,11 @@ def parse():
     ap.add_argument("--copy-reference-mib", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB, a "
                          "reference of known size for hardware byte counters")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="(no GPU) read the counter_collection.csv files of a rocprofv3 "
+                         "--pmc FETCH_SIZE run and a --pmc WRITE_SIZE run of this script "
+                         "(with --copy-reference-mib) and record HBM bytes per launch in "
+                         + os.path.relpath(TRAFFIC_FILE, ROOT))
     return ap.parse_args()
 
 
@@ -68,6 +73,57 @@ def measured_traffic(workload: str):
     if rec.get("workload") != workload or rec.get("source_sha256_16") != source_hash(FWD_SOURCE):
         return None
     return rec.get("bytes_per_launch")
+
+
+KERNELS = {"sparse_fwd": "sparse_fwd_bf16_kernel", "transpose_v": "transpose_v_kernel",
+           "calibrate": "calib_bf16_kernel", "select_rows": "select_rows_kernel",
+           "compact_rows": "compact_rows_kernel"}
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _counter_per_dispatch(path: str, counter: str):
+    """{dispatch id: (kernel name, value in KiB)} of one rocprofv3 counter CSV."""
+    import csv
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            d = int(r["Dispatch_Id"])
+            name, val = out.get(d, (r["Kernel_Name"], 0.0))
+            out[d] = (name, val + float(r["Counter_Value"]))
+    return out
+
+
+def record_traffic(fetch_csv: str, write_csv: str, copy_mib: int, workload: str):
+    """HBM bytes per launch from FETCH_SIZE / WRITE_SIZE, each scaled by what the
+    same counter reads for the reference copy of copy_mib MiB (read and written
+    once).  Written to TRAFFIC_FILE with the hash of the kernel source."""
+    if copy_mib <= 0:
+        sys.exit("--record-traffic needs the --copy-reference-mib the counter runs used")
+    res = {"workload": workload, "source_sha256_16": source_hash(FWD_SOURCE),
+           "copy_reference_mib": copy_mib, "kernels": {}}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        per = _counter_per_dispatch(path, counter)
+        copies = [v for n, v in per.values() if n == COPY_KERNEL]
+        if not copies:
+            sys.exit(f"{path}: no {COPY_KERNEL} dispatch (run with --copy-reference-mib)")
+        scale = copy_mib * 1024.0 / max(copies)   # known KiB / counted KiB
+        res[counter.lower() + "_scale"] = round(scale, 4)
+        for key, pat in KERNELS.items():
+            vals = [v for n, v in per.values() if pat in n]
+            if vals:
+                k = res["kernels"].setdefault(key, {"launches": len(vals)})
+                k[counter.lower().replace("_size", "_bytes")] = int(sum(vals) / len(vals) * scale * 1024)
+    fwd = res["kernels"].get("sparse_fwd", {})
+    if "fetch_bytes" not in fwd or "write_bytes" not in fwd:
+        sys.exit("no sparse forward dispatch in the counter files")
+    res["bytes_per_launch"] = fwd["fetch_bytes"] + fwd["write_bytes"]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(res, f, indent=1)
+        f.write("\n")
+    print(json.dumps(res))
 
 
 def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
@@ -105,6 +161,9 @@ def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
 
 def main():
     args = parse()
+    if args.record_traffic:
+        record_traffic(*args.record_traffic, args.copy_reference_mib, args.workload)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "bench.py measures one GPU only: every GPU box here has one "
