@@ -33,7 +33,7 @@ if ROOT not in sys.path:
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix-core peak
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_fwd_traffic.json")
-FWD_SOURCE = os.path.join(ROOT, "paper_2608_12032_amd", "csrc", "sparse_fwd.hip")
+CSRC = os.path.join(ROOT, "paper_2608_12032_amd", "csrc")
 
 
 def parse():
@@ -58,21 +58,25 @@ def parse():
     return ap.parse_args()
 
 
-def source_hash(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_hash() -> str:
+    """Hash of every kernel source of the library (HIP, headers, C ABI)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per launch of the sparse forward, from the rocprofv3 counter
-    runs recorded under profiles/, if they were taken on the current kernel."""
+    """Per-kernel HBM bytes per launch from the rocprofv3 counter runs recorded
+    under profiles/, if they were taken on the current kernel sources."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if rec.get("workload") != workload or rec.get("source_sha256_16") != source_hash(FWD_SOURCE):
+    if rec.get("workload") != workload or rec.get("source_sha256_16") != source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec
 
 
 KERNELS = {"sparse_fwd": "sparse_fwd_bf16_kernel", "transpose_v": "transpose_v_kernel",
@@ -101,7 +105,7 @@ def record_traffic(fetch_csv: str, write_csv: str, copy_mib: int, workload: str)
     once).  Written to TRAFFIC_FILE with the hash of the kernel source."""
     if copy_mib <= 0:
         sys.exit("--record-traffic needs the --copy-reference-mib the counter runs used")
-    res = {"workload": workload, "source_sha256_16": source_hash(FWD_SOURCE),
+    res = {"workload": workload, "source_sha256_16": source_hash(),
            "copy_reference_mib": copy_mib, "kernels": {}}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         per = _counter_per_dispatch(path, counter)
@@ -245,6 +249,25 @@ def main():
     dense_flop = 4.0 * w.B * w.H * N * N * d
     achieved = retained_flop / (fwd * 1e-3) / 1e12
     traffic = measured_traffic(args.workload)
+    n_pad = w.N_pad
+    # algorithmic bytes per launch
+    elt = 2 if w.dtype == "bf16" else 4
+    qkv = w.B * w.H * n_pad * d * elt
+    mass_b = w.B * w.H * n_q * n_k * 4
+    alg = {"sparse_fwd": 4 * qkv + 4 * (rows + 1 + nnz),
+           "calibrate": 2 * qkv + mass_b,
+           "select": mass_b + 4 * (rows + 1 + nnz)}
+    cal_t = sum(cal_ms) / len(cal_ms)
+    sel_t = sum(sel_ms) / len(sel_ms)
+    hbm = {"calibrate": {"algorithmic_GBs": round(alg["calibrate"] / cal_t / 1e6, 1)},
+           "select": {"algorithmic_GBs": round(alg["select"] / sel_t / 1e6, 1)},
+           "note": "algorithmic bytes / measured time; counted_GBs = rocprofv3 FETCH_SIZE + "
+                   "WRITE_SIZE bytes (scaled by a reference copy) / measured time"}
+    if traffic:
+        kb = traffic["kernels"]
+        tot = lambda key: kb.get(key, {}).get("fetch_bytes", 0) + kb.get(key, {}).get("write_bytes", 0)  # noqa: E731
+        hbm["calibrate"]["counted_GBs"] = round(tot("calibrate") / cal_t / 1e6, 1)
+        hbm["select"]["counted_GBs"] = round((tot("select_rows") + tot("compact_rows")) / sel_t / 1e6, 1)
 
     res = {
         "metric": "ms/layer + fraction of bf16 MFMA peak, block-sparse attn fwd, Wan-shaped tau=0.99",
@@ -280,8 +303,10 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": traffic,
+            "traffic": traffic["bytes_per_launch"] if traffic else None,
+            "traffic_algorithmic": alg["sparse_fwd"],
         },
+        "hbm": hbm,
     }
     if not args.no_cpu_baseline:
         q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)
