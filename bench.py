@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--workload", default="wan", choices=["wan", "cog", "hunyuan", "tiny"])
     ap.add_argument("--reuse", type=int, default=None, help="override the reuse-step count")
     ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--block-k", type=int, default=0,
+                    help="key block size when it differs from the query block (32: the "
+                         "paper's rectangular 128 x 32 setting)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -147,13 +150,13 @@ def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
     rows = rp_h.size - 1
     order = np.random.default_rng(0).permutation(rows)
     t0 = time.perf_counter()
-    O.sparse_attention(qh, kh, vh, w.N, w.block, w.block, w.scale, rp_h, ci_h,
+    O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
                        rows_subset=order[:4])
     per_row = (time.perf_counter() - t0) / 4
     n = int(min(rows, max(8, budget_s / max(per_row, 1e-6))))
     sample = order[:n]
     t0 = time.perf_counter()
-    O.sparse_attention(qh, kh, vh, w.N, w.block, w.block, w.scale, rp_h, ci_h,
+    O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
                        rows_subset=sample)
     dt = time.perf_counter() - t0
     ms_layer = dt / n * rows * 1e3
@@ -184,10 +187,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     w = W.WORKLOADS[args.workload]
+    if args.block_k:
+        w = W.rectangular(w, args.block_k)
     tau = w.tau if args.tau is None else args.tau
     reuse = w.reuse if args.reuse is None else args.reuse
-    N, C, d = w.N, w.block, w.d
-    n_q = n_k = w.n_blocks
+    N, C, Ck, d = w.N, w.block, w.bk, w.d
+    n_q, n_k = w.n_blocks, w.n_kblocks
     rows = w.B * w.H * n_q
 
     # ---- inputs resident in HBM before timing --------------------------------
@@ -202,10 +207,10 @@ def main():
     mass = torch.empty((w.B, w.H, n_q, n_k), dtype=torch.float32, device=dev)
     row_ptr = torch.empty(rows + 1, dtype=torch.int32, device=dev)
     col_idx = torch.empty(rows * n_k, dtype=torch.int32, device=dev)
-    ws_sel = torch.empty(max(L.workspace_bytes(1, 0, w.B, w.H, N, 1, C, C), 16),
+    ws_sel = torch.empty(max(L.workspace_bytes(1, 0, w.B, w.H, N, 1, C, Ck), 16),
                          dtype=torch.uint8, device=dev)
     ws_fwd = torch.empty(max(L.workspace_bytes(2, 1 if w.dtype == "bf16" else 0, w.B, w.H, N, d,
-                                               C, C), 16), dtype=torch.uint8, device=dev)
+                                               C, Ck), 16), dtype=torch.uint8, device=dev)
     out = torch.empty_like(q0)
     if args.copy_reference_mib > 0:
         nbytes = args.copy_reference_mib << 20
@@ -220,14 +225,14 @@ def main():
     def step():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 + 2 * reuse)]
         ev[0].record()
-        L.losa_calibrate_mass(q0, k0, N, C, want_lse=False, mass=mass)
+        L.losa_calibrate_mass(q0, k0, N, C, Ck, want_lse=False, mass=mass)
         ev[1].record()
-        L.losa_select_blocks(mass, N, C, C, tau, row_ptr=row_ptr, col_idx=col_idx,
+        L.losa_select_blocks(mass, N, C, Ck, tau, row_ptr=row_ptr, col_idx=col_idx,
                              workspace=ws_sel)
         ev[2].record()
         for t, (q, k, v) in enumerate(reuse_inputs):
             ev[3 + 2 * t].record()
-            L.losa_sparse_attn_fwd(q, k, v, N, C, C, row_ptr, col_idx, out=out, workspace=ws_fwd)
+            L.losa_sparse_attn_fwd(q, k, v, N, C, Ck, row_ptr, col_idx, out=out, workspace=ws_fwd)
             ev[4 + 2 * t].record()
         return ev
 
@@ -245,10 +250,11 @@ def main():
     nnz = L.nnz(row_ptr)
     fwd = sum(fwd_ms) / len(fwd_ms)
     fwd_sorted = sorted(fwd_ms)
-    retained_flop = 4.0 * C * C * d * nnz
+    retained_flop = 4.0 * C * Ck * d * nnz
     dense_flop = 4.0 * w.B * w.H * N * N * d
     achieved = retained_flop / (fwd * 1e-3) / 1e12
-    traffic = measured_traffic(args.workload)
+    wkey = args.workload + (f"-c{Ck}" if Ck != C else "")
+    traffic = measured_traffic(wkey)
     n_pad = w.N_pad
     # algorithmic bytes per launch
     elt = 2 if w.dtype == "bf16" else 4
@@ -284,7 +290,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}-shaped: B={w.B} H={w.H} d={d} N={N} (padded {w.N_pad}) "
-                        f"grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]} block {C} tau={tau}",
+                        f"grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]} "
+                        + (f"block {C}" if Ck == C else f"blocks {C}x{Ck}") + f" tau={tau}",
             "step": f"calibrate + select + {reuse} reuse sparse forwards",
             "reuse_steps": reuse,
             "nnz_blocks": nnz,

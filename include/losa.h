@@ -25,8 +25,10 @@
  * - Validation is synchronous and happens before any HIP call: on an error
  *   nothing is launched, outputs are untouched, and losa_last_error() holds a
  *   description.  Launch failures return LOSA_ERR_HIP.
- * - Supported (v1): dtype BF16 or F32, d in {64, 128}, block_q == block_k in
- *   {64, 128}.  Other valid combinations return LOSA_ERR_UNSUPPORTED.
+ * - Supported: dtype BF16 or F32, d in {64, 128}, block_q in {64, 128} and
+ *   block_k either equal to block_q or 32 (the paper's rectangular setting,
+ *   Sec. 5.1: 128-row query blocks, 32-key key blocks).  Other valid
+ *   combinations return LOSA_ERR_UNSUPPORTED.
  * - Calls are deterministic: the same inputs give bitwise identical outputs.
  */
 #ifndef LOSA_H

@@ -66,10 +66,10 @@ losa_status check_supported(losa_dtype dtype, const Shape& s) {
     return fail(LOSA_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
   if (s.d != 64 && s.d != 128)
     return fail(LOSA_ERR_UNSUPPORTED, "head dim d=%d not supported (64 or 128)", s.d);
-  if (s.bq != s.bk)
-    return fail(LOSA_ERR_UNSUPPORTED, "block_q=%d != block_k=%d not supported", s.bq, s.bk);
   if (s.bq != 64 && s.bq != 128)
-    return fail(LOSA_ERR_UNSUPPORTED, "block %d not supported (64 or 128)", s.bq);
+    return fail(LOSA_ERR_UNSUPPORTED, "block_q=%d not supported (64 or 128)", s.bq);
+  if (s.bk != s.bq && s.bk != 32)
+    return fail(LOSA_ERR_UNSUPPORTED, "block_k=%d not supported (block_q=%d, or 32)", s.bk, s.bq);
   return LOSA_OK;
 }
 
@@ -108,11 +108,12 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
       return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks exceed the calibration LDS budget",
                   s.n_k);
     return hip_status(
-        losa::launch_calibrate_bf16(d, block_q, q, k, B, H, N, s.n_pad, scale, mass, lse, hs),
+        losa::launch_calibrate_bf16(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale, mass, lse,
+                                    hs),
         "losa_calibrate_mass");
   }
   return hip_status(
-      losa::launch_calibrate_f32(d, block_q, q, k, B, H, N, s.n_pad, scale, mass, lse, hs),
+      losa::launch_calibrate_f32(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale, mass, lse, hs),
       "losa_calibrate_mass");
 }
 
@@ -177,12 +178,12 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
     if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
     if (workspace_bytes < need)
       return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
-    return hip_status(losa::launch_sparse_fwd_bf16(d, block_q, q, k, v, B, H, N, s.n_pad, scale,
+    return hip_status(losa::launch_sparse_fwd_bf16(d, block_q, block_k, q, k, v, B, H, N, s.n_pad, scale,
                                                    row_ptr, col_idx, col_idx_len, o, lse,
                                                    workspace, hs),
                       "losa_sparse_attn_fwd");
   }
-  return hip_status(losa::launch_sparse_fwd_f32(d, block_q, q, k, v, B, H, N, s.n_pad, scale,
+  return hip_status(losa::launch_sparse_fwd_f32(d, block_q, block_k, q, k, v, B, H, N, s.n_pad, scale,
                                                 row_ptr, col_idx, col_idx_len, o, lse, hs),
                     "losa_sparse_attn_fwd");
 }

@@ -5,6 +5,9 @@
 //   mbar(i, j) = (1 / R_i) * sum_{q in B_i, q < N} sum_{k in B_j, k < N}
 //                exp(s_qk - lse_q),     s = scale * q . k,
 // i.e. Eq. (1)'s M(i, j) divided by R_i, so every row of mbar sums to one.
+// Query blocks have BLK rows, key blocks BK keys (BK = BLK, or 32 for the
+// paper's rectangular setting with 128-row query blocks and 32-key key blocks);
+// the keys stream through LDS in tiles of BLK keys either way.
 //
 // The normaliser lse_q is known only after all keys are seen, so a workgroup
 // (one query block, BLK/32 waves of 32 query rows) makes two sweeps over the
@@ -30,7 +33,7 @@ struct CalCfg {
   static constexpr int NW = BLK / 32;
   static constexpr int NT = NW * 64;
   static constexpr int KS = D / 16;
-  static constexpr int KB = BLK / 32;
+  static constexpr int KB = BLK / 32;                // 32-key sub-blocks of a tile
   static constexpr int KROW = D * 2;
   static constexpr int KCH = D / 8;
   static constexpr int TILE = BLK * D * 2;
@@ -74,12 +77,15 @@ __device__ __forceinline__ void tile_scores(const char* buf, const bf16x8_t* qre
   }
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 __global__ void __launch_bounds__(BLK * 2, 2)
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                       float* __restrict__ mass, float* __restrict__ lse, int rows_total, int n_q,
                       int n_k, int N, int n_pad, float scale_log2) {
   using C = CalCfg<D, BLK>;
+  static_assert(BK % 32 == 0 && BLK % BK == 0, "key blocks split a tile into whole sub-blocks");
+  constexpr int TB = BLK / BK;   // key blocks per tile
+  constexpr int SPB = BK / 32;   // 32-key sub-blocks per key block
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   char* buf0 = smem;
   char* buf1 = smem + C::TILE;
@@ -113,7 +119,7 @@ __global__ void __launch_bounds__(BLK * 2, 2)
 #pragma unroll
     for (int s = 0; s < C::KS; ++s) qreg[s] = qp[2 * s + g];
   }
-  const int n_kv = (N + BLK - 1) / BLK;  // key blocks holding a real key
+  const int n_kv = (N + BLK - 1) / BLK;  // key tiles holding a real key
 
   // ---- sweep 1: running max / sum -> lse (log2 units) ----------------------
   float m_run = kNegBig;
@@ -165,23 +171,29 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     f32x16_t sacc[C::KB];
     tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
-    float acc = 0.f;
+    float acc[TB];
+#pragma unroll
+    for (int b = 0; b < TB; ++b) acc[b] = 0.f;
 #pragma unroll
     for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
         const int key = kb * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
         const float x = key < kvalid ? sacc[kb][t] * scale_log2 : -INFINITY;
-        acc += fast_exp2(x - sub);
+        acc[kb / SPB] += fast_exp2(x - sub);
       }
-    acc = wave_sum(acc);
-    if (lane == 0) part[w * n_k + j] = acc;
+#pragma unroll
+    for (int b = 0; b < TB; ++b) {
+      const float a = wave_sum(acc[b]);
+      if (lane == 0) part[w * n_k + j * TB + b] = a;
+    }
   }
   lds_read_barrier();  // partials written (lgkmcnt covers the LDS stores)
   const float inv_rows = 1.0f / (float)rows_valid;
+  const int n_kb = n_kv * TB;  // key blocks inside the tiles swept (the rest hold no key)
   for (int j = tid; j < n_k; j += C::NT) {
     float s = 0.f;
-    if (j < n_kv) {
+    if (j < n_kb) {
 #pragma unroll
       for (int ww = 0; ww < C::NW; ++ww) s += part[ww * n_k + j];
     }
@@ -189,18 +201,19 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   }
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 hipError_t launch_cal(const void* q, const void* k, int B, int H, int N, int n_pad, float scale,
                       float* mass, float* lse, hipStream_t stream) {
   using C = CalCfg<D, BLK>;
   const int n_q = n_pad / BLK;
-  const int n_k = n_pad / BLK;
+  const int n_k = n_pad / BK;
   const int rows = B * H * n_q;
   const size_t lds = 2 * (size_t)C::TILE + (size_t)C::NW * n_k * sizeof(float);
-  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t err =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK, BK>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK>), dim3(rows), dim3(C::NT), lds, stream,
+  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(C::NT), lds, stream,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), mass, lse,
                      rows, n_q, n_k, N, n_pad, scale * kLog2e);
   return hipGetLastError();
@@ -212,14 +225,21 @@ size_t calib_bf16_lds_bytes(int d, int blk, int n_k) {
   return 2 * (size_t)blk * d * 2 + (size_t)(blk / 32) * n_k * sizeof(float);
 }
 
-hipError_t launch_calibrate_bf16(int d, int blk, const void* q, const void* k, int B, int H, int N,
-                                 int n_pad, float scale, float* mass, float* lse,
+hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
+                                 int H, int N, int n_pad, float scale, float* mass, float* lse,
                                  hipStream_t stream) {
-  if (d == 128 && blk == 128)
-    return launch_cal<128, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 64 && blk == 128) return launch_cal<64, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 128 && blk == 64) return launch_cal<128, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 64 && blk == 64) return launch_cal<64, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+#define LOSA_CAL(DD, BB, KK)                                                              \
+  if (d == DD && blk == BB && blk_k == KK)                                                \
+    return launch_cal<DD, BB, KK>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  LOSA_CAL(128, 128, 128)
+  LOSA_CAL(64, 128, 128)
+  LOSA_CAL(128, 64, 64)
+  LOSA_CAL(64, 64, 64)
+  LOSA_CAL(128, 128, 32)
+  LOSA_CAL(64, 128, 32)
+  LOSA_CAL(128, 64, 32)
+  LOSA_CAL(64, 64, 32)
+#undef LOSA_CAL
   return hipErrorInvalidValue;
 }
 

@@ -3,8 +3,9 @@
 //
 // fp32 is the small-workload path (no bf16 rounding anywhere), so these
 // kernels keep to a plain layout: one thread per query row, one workgroup per
-// query block, key/value rows staged through LDS in chunks of 32 keys and read
-// by every thread as broadcasts.  Masking and padding follow the bf16 kernels:
+// query block of BLK rows, key/value rows of a key block (BK keys: BLK, or 32)
+// staged through LDS in chunks of 32 keys and read by every thread as
+// broadcasts.  Masking and padding follow the bf16 kernels:
 // keys >= N never enter a softmax, query rows >= N get O = 0 and lse = -inf,
 // and so do rows whose key set is empty; col_idx entries outside [0, n_k) are
 // ignored, a repeated entry counts once (the row's ids are flagged in LDS and
@@ -29,7 +30,7 @@ __device__ __forceinline__ void stage_rows(float* dst, const float* src, int key
   }
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 __global__ void __launch_bounds__(BLK)
     sparse_fwd_f32_kernel(const float* __restrict__ Q, const float* __restrict__ K,
                           const float* __restrict__ V, const int32_t* __restrict__ row_ptr,
@@ -66,11 +67,11 @@ __global__ void __launch_bounds__(BLK)
   __syncthreads();
   for (int j = 0; j < n_k; ++j) {
     if (!flag[j]) continue;  // the same LDS value for every thread
-    const int kvalid = min(BLK, N - j * BLK);
+    const int kvalid = min(BK, N - j * BK);
     for (int c0 = 0; c0 < kvalid; c0 += CK) {
       __syncthreads();
-      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
-      stage_rows<D, BLK>(Vc, V + head, j * BLK + c0, t);
+      stage_rows<D, BLK>(Kc, K + head, j * BK + c0, t);
+      stage_rows<D, BLK>(Vc, V + head, j * BK + c0, t);
       __syncthreads();
       const int nk = min(CK, kvalid - c0);
       float s[CK];
@@ -104,7 +105,7 @@ __global__ void __launch_bounds__(BLK)
   if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = ok ? (m + __log2f(l)) * kLn2 : -INFINITY;
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 __global__ void __launch_bounds__(BLK)
     calib_f32_kernel(const float* __restrict__ Q, const float* __restrict__ K,
                      float* __restrict__ mass, float* __restrict__ lse, int n_q, int n_k, int N,
@@ -128,15 +129,15 @@ __global__ void __launch_bounds__(BLK)
   float q[D];
 #pragma unroll
   for (int dd = 0; dd < D; ++dd) q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
-  const int n_kv = (N + BLK - 1) / BLK;
+  const int n_kv = (N + BK - 1) / BK;  // key blocks holding a real key
 
   // sweep 1: running max / sum over every valid key
   float m = kNegBig, l = 0.f;
   for (int j = 0; j < n_kv; ++j) {
-    const int kvalid = min(BLK, N - j * BLK);
+    const int kvalid = min(BK, N - j * BK);
     for (int c0 = 0; c0 < kvalid; c0 += CK) {
       __syncthreads();
-      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
+      stage_rows<D, BLK>(Kc, K + head, j * BK + c0, t);
       __syncthreads();
       const int nk = min(CK, kvalid - c0);
       float s[CK];
@@ -164,11 +165,11 @@ __global__ void __launch_bounds__(BLK)
   const int lane = t & 63, w = t >> 6;
   const float inv_rows = 1.0f / (float)rows_valid;
   for (int j = 0; j < n_kv; ++j) {
-    const int kvalid = min(BLK, N - j * BLK);
+    const int kvalid = min(BK, N - j * BK);
     float acc = 0.f;
     for (int c0 = 0; c0 < kvalid; c0 += CK) {
       __syncthreads();
-      stage_rows<D, BLK>(Kc, K + head, j * BLK + c0, t);
+      stage_rows<D, BLK>(Kc, K + head, j * BK + c0, t);
       __syncthreads();
       const int nk = min(CK, kvalid - c0);
 #pragma unroll
@@ -192,23 +193,23 @@ __global__ void __launch_bounds__(BLK)
   for (int j = n_kv + t; j < n_k; j += BLK) mrow[j] = 0.f;
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 hipError_t launch_f32(const void* q, const void* k, const void* v, int B, int H, int N, int n_pad,
                       float scale, const int32_t* row_ptr, const int32_t* col_idx,
                       int64_t col_len, void* o, float* lse, hipStream_t stream) {
-  const int n_q = n_pad / BLK, n_k = n_pad / BLK;
-  hipLaunchKernelGGL((sparse_fwd_f32_kernel<D, BLK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
+  const int n_q = n_pad / BLK, n_k = n_pad / BK;
+  hipLaunchKernelGGL((sparse_fwd_f32_kernel<D, BLK, BK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
                      static_cast<const float*>(q), static_cast<const float*>(k),
                      static_cast<const float*>(v), row_ptr, col_idx, col_len,
                      static_cast<float*>(o), lse, n_q, n_k, N, n_pad, scale * kLog2e);
   return hipGetLastError();
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 hipError_t launch_cal_f32(const void* q, const void* k, int B, int H, int N, int n_pad, float scale,
                           float* mass, float* lse, hipStream_t stream) {
-  const int n_q = n_pad / BLK, n_k = n_pad / BLK;
-  hipLaunchKernelGGL((calib_f32_kernel<D, BLK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
+  const int n_q = n_pad / BLK, n_k = n_pad / BK;
+  hipLaunchKernelGGL((calib_f32_kernel<D, BLK, BK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
                      static_cast<const float*>(q), static_cast<const float*>(k), mass, lse, n_q,
                      n_k, N, n_pad, scale * kLog2e);
   return hipGetLastError();
@@ -216,29 +217,41 @@ hipError_t launch_cal_f32(const void* q, const void* k, int B, int H, int N, int
 
 }  // namespace
 
-hipError_t launch_sparse_fwd_f32(int d, int blk, const void* q, const void* k, const void* v,
-                                 int B, int H, int N, int n_pad, float scale,
+hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const void* k,
+                                 const void* v, int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
                                  void* o, float* lse, hipStream_t stream) {
-#define LOSA_F32_FWD(DD, BB)                                                                 \
-  if (d == DD && blk == BB)                                                                  \
-    return launch_f32<DD, BB>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, \
-                              lse, stream);
-  LOSA_F32_FWD(64, 64)
-  LOSA_F32_FWD(64, 128)
-  LOSA_F32_FWD(128, 64)
-  LOSA_F32_FWD(128, 128)
+#define LOSA_F32_FWD(DD, BB, KK)                                                               \
+  if (d == DD && blk == BB && blk_k == KK)                                                     \
+    return launch_f32<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, \
+                                  lse, stream);
+  LOSA_F32_FWD(64, 64, 64)
+  LOSA_F32_FWD(64, 128, 128)
+  LOSA_F32_FWD(128, 64, 64)
+  LOSA_F32_FWD(128, 128, 128)
+  LOSA_F32_FWD(64, 64, 32)
+  LOSA_F32_FWD(64, 128, 32)
+  LOSA_F32_FWD(128, 64, 32)
+  LOSA_F32_FWD(128, 128, 32)
 #undef LOSA_F32_FWD
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_calibrate_f32(int d, int blk, const void* q, const void* k, int B, int H, int N,
-                                int n_pad, float scale, float* mass, float* lse,
+hipError_t launch_calibrate_f32(int d, int blk, int blk_k, const void* q, const void* k, int B,
+                                int H, int N, int n_pad, float scale, float* mass, float* lse,
                                 hipStream_t stream) {
-  if (d == 64 && blk == 64) return launch_cal_f32<64, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 64 && blk == 128) return launch_cal_f32<64, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 128 && blk == 64) return launch_cal_f32<128, 64>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
-  if (d == 128 && blk == 128) return launch_cal_f32<128, 128>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+#define LOSA_F32_CAL(DD, BB, KK)                                                              \
+  if (d == DD && blk == BB && blk_k == KK)                                                    \
+    return launch_cal_f32<DD, BB, KK>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+  LOSA_F32_CAL(64, 64, 64)
+  LOSA_F32_CAL(64, 128, 128)
+  LOSA_F32_CAL(128, 64, 64)
+  LOSA_F32_CAL(128, 128, 128)
+  LOSA_F32_CAL(64, 64, 32)
+  LOSA_F32_CAL(64, 128, 32)
+  LOSA_F32_CAL(128, 64, 32)
+  LOSA_F32_CAL(128, 128, 32)
+#undef LOSA_F32_CAL
   return hipErrorInvalidValue;
 }
 

@@ -15,11 +15,12 @@ __host__ __device__ inline int padded_len(int N, int block_q, int block_k) {
   return (N + L - 1) / L * L;
 }
 
-hipError_t launch_calibrate_bf16(int d, int blk, const void* q, const void* k, int B, int H, int N,
-                                 int n_pad, float scale, float* mass, float* lse,
+// blk = query block rows, blk_k = key block keys (blk, or 32)
+hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
+                                 int H, int N, int n_pad, float scale, float* mass, float* lse,
                                  hipStream_t stream);
-hipError_t launch_calibrate_f32(int d, int blk, const void* q, const void* k, int B, int H, int N,
-                                int n_pad, float scale, float* mass, float* lse,
+hipError_t launch_calibrate_f32(int d, int blk, int blk_k, const void* q, const void* k, int B,
+                                int H, int N, int n_pad, float scale, float* mass, float* lse,
                                 hipStream_t stream);
 size_t calib_bf16_lds_bytes(int d, int blk, int n_k);
 
@@ -29,13 +30,13 @@ hipError_t launch_select(const float* mass, int B, int H, int N, int block_q, in
 size_t select_workspace_bytes(int rows, int n_k);
 int select_max_nk();
 
-hipError_t launch_sparse_fwd_bf16(int d, int blk, const void* q, const void* k, const void* v,
-                                  int B, int H, int N, int n_pad, float scale,
+hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, const void* k,
+                                  const void* v, int B, int H, int N, int n_pad, float scale,
                                   const int32_t* row_ptr, const int32_t* col_idx,
                                   int64_t col_len, void* o, float* lse, void* workspace,
                                   hipStream_t stream);
-hipError_t launch_sparse_fwd_f32(int d, int blk, const void* q, const void* k, const void* v,
-                                 int B, int H, int N, int n_pad, float scale,
+hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const void* k,
+                                 const void* v, int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
                                  void* o, float* lse, hipStream_t stream);
 size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d, int n_q);

@@ -74,13 +74,13 @@ __device__ __forceinline__ int perm16(int p) {
   return (q2 << 2) | (p & 3);
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 struct FwdCfg {
   static constexpr int NW = BLK / 32;                // waves per workgroup
   static constexpr int NT = NW * 64;                 // threads
   static constexpr int KS = D / 16;                  // k-steps of S^T = K Q^T
   static constexpr int DB = D / 32;                  // 32-row d sub-blocks of O^T
-  static constexpr int NS = BLK / 32;                // 32-key sub-tiles per key block
+  static constexpr int NS = BK / 32;                 // 32-key sub-tiles per key block
   static constexpr int R = kRing;                    // slots per ring
   static constexpr int BPI = R / NS;                 // key blocks per unrolled loop pass
   static constexpr int SUB = 32 * D * 2;             // bytes of a K or V^T sub-tile
@@ -97,9 +97,9 @@ struct FwdCfg {
 };
 
 // Swizzled chunk of K chunk c in sub-tile row `row`.
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 __device__ __forceinline__ int kswz(int row, int c) {
-  using C = FwdCfg<D, BLK>;
+  using C = FwdCfg<D, BLK, BK>;
   return c ^ ((row / C::KRPL) % C::KCPR);
 }
 
@@ -161,11 +161,11 @@ __device__ __forceinline__ void launder(uint32_t& x) { asm volatile("" : "+v"(x)
 // sub-tile (PV); the prologue and the drain of the pipeline.  ka[st] is this
 // lane's LDS address of its chunk for k-step st in K slot 0, va[st] the same
 // in V^T slot 0; kimm / vimm select the slot.
-template <int D, int BLK, bool QK, bool PV>
+template <int D, int BLK, int BK, bool QK, bool PV>
 __device__ __forceinline__ void mfma_pair(const uint32_t* ka, uint32_t kimm, const bf16x8_t* qreg,
                                           f32x16_t& snext, const uint32_t* va, uint32_t vimm,
                                           const bf16x8_t* pprev, f32x16_t* o) {
-  using C = FwdCfg<D, BLK>;
+  using C = FwdCfg<D, BLK, BK>;
   constexpr int NPV = 2 * C::DB;
 #pragma unroll
   for (int i = 0; i < C::KS; ++i) {
@@ -211,14 +211,14 @@ __device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_lo
 // sums.  The NL global->LDS loads of this sub-iteration (issue(t), t < NL)
 // are spread evenly over the MFMAs instead of leaving in one burst.
 // sched_group_barrier fixes this order.
-template <int D, int BLK, int NPRE, int NL, typename Issue>
+template <int D, int BLK, int BK, int NPRE, int NL, typename Issue>
 __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm,
                                                const bf16x8_t* qreg, f32x16_t& snext,
                                                const uint32_t* va, uint32_t vimm,
                                                const bf16x8_t* pprev, f32x16_t* o, f32x16_t& cur,
                                                float scale_log2, float m_run, bf16x8_t* pcur,
                                                Issue&& issue) {
-  using C = FwdCfg<D, BLK>;
+  using C = FwdCfg<D, BLK, BK>;
   constexpr int NM = C::KS + 2 * C::DB;
   static_assert(NM == 16 || NM == 8, "softmax split written for 8 or 16 MFMAs");
   static_assert(NL <= NM, "at most one load per MFMA");
@@ -310,7 +310,7 @@ __device__ __forceinline__ void mask_sub(f32x16_t& s, int part, int kvalid, int 
 // (at most 2^20 per key over at most 2^19 keys).
 constexpr float kSumBound = 1048576.0f;
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 __global__ void __launch_bounds__(BLK * 2)
     __attribute__((amdgpu_waves_per_eu(BLK == 128 ? 2 : 1)))
     sparse_fwd_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
@@ -319,7 +319,7 @@ __global__ void __launch_bounds__(BLK * 2)
                            __bf16* __restrict__ O, float* __restrict__ lse,
                            const int* __restrict__ order, int n_q, int n_k, int N, int n_pad,
                            float scale_log2) {
-  using C = FwdCfg<D, BLK>;
+  using C = FwdCfg<D, BLK, BK>;
   constexpr int NS = C::NS;
   constexpr int R = C::R;
   constexpr int BPI = C::BPI;
@@ -378,7 +378,12 @@ __global__ void __launch_bounds__(BLK * 2)
     }
     nb = __builtin_amdgcn_readfirstlane(nb);
   }
-  const int S = nb * NS;  // sub-tiles in the stream
+  // sub-tiles in the stream.  With 32-key blocks (one sub-tile each) the
+  // stream is padded to whole loop passes with sub-tiles whose keys are all
+  // masked (they add nothing to O or l); larger blocks fill passes exactly,
+  // or leave half a pass that the loop stops after.
+  const int S_real = nb * NS;
+  const int S = (NS == 1) ? (S_real + R - 1) / R * R : S_real;
 
   // this lane's query row and its Q^T operand (8 bf16 per k-step)
   const int qrow = qb * BLK + w * 32 + l32;
@@ -394,7 +399,7 @@ __global__ void __launch_bounds__(BLK * 2)
   uint32_t ka[C::KS], va[2];
 #pragma unroll
   for (int st = 0; st < C::KS; ++st)
-    ka[st] = lds0 + l32 * C::KROW + (kswz<D, BLK>(l32, 2 * st + g) << 4);
+    ka[st] = lds0 + l32 * C::KROW + (kswz<D, BLK, BK>(l32, 2 * st + g) << 4);
 #pragma unroll
   for (int st = 0; st < 2; ++st)
     va[st] = lds0 + C::RING + (l32 >> 2) * 256 +
@@ -407,7 +412,7 @@ __global__ void __launch_bounds__(BLK * 2)
   for (int u = 0; u < C::LPW; ++u) {
     const int o = (w * C::LPW + u) * 1024 + lane * 16;
     const int row = o / C::KROW;
-    koffs[u] = (uint32_t)(row * C::KROW + (kswz<D, BLK>(row, (o % C::KROW) >> 4) << 4));
+    koffs[u] = (uint32_t)(row * C::KROW + (kswz<D, BLK, BK>(row, (o % C::KROW) >> 4) << 4));
   }
   const uint32_t voff0 = (uint32_t)(w * C::LPW * 1024 + lane * 16);
 
@@ -416,7 +421,7 @@ __global__ void __launch_bounds__(BLK * 2)
 #pragma unroll
     for (int u = 0; u < C::LPW; ++u)
       dma16(lds0 + x * C::SUB + (w * C::LPW + u) * 1024, krs, koffs[u],
-            (uint32_t)((j * BLK + part * 32) * C::KROW));
+            (uint32_t)((j * BK + part * 32) * C::KROW));
   };
   auto load_v = [&](int x, int j, int part) {
 #pragma unroll
@@ -439,8 +444,10 @@ __global__ void __launch_bounds__(BLK * 2)
 
   if (S > 0) {
     int jc[BPI], jn[BPI];  // blocks of this loop pass's sub-tiles and the next pass's
-    // prologue: K sub-tiles 0..R-1, V^T sub-tiles 0..R-3; zero V^T slot R-1
-    // and the probabilities of "sub-tile -1"; scores of sub-tile 0
+    // prologue: K sub-tiles 0..R-1, V^T sub-tiles 0..R-3 (past the end of
+    // the stream the last block again, so that no slot holds stale bytes);
+    // zero V^T slot R-1 and the probabilities of "sub-tile -1"; scores of
+    // sub-tile 0
 #pragma unroll
     for (int x = 0; x < BPI; ++x) {
       jc[x] = block_at(x);
@@ -449,8 +456,8 @@ __global__ void __launch_bounds__(BLK * 2)
 #pragma unroll
     for (int y = 0; y < R; ++y) {
       const int jy = (y / NS < BPI) ? jc[y / NS] : jn[y / NS - BPI];
-      if (y < S) load_k(y, jy, y % NS);
-      if (y < R - 2 && y < S) load_v(y, jy, y % NS);
+      load_k(y, jy, y % NS);
+      if (y < R - 2) load_v(y, jy, y % NS);
     }
     for (int x = tid * 16; x < C::SUB; x += C::NT * 16)
       *reinterpret_cast<f32x4_t*>(smem + C::RING + (R - 1) * C::SUB + x) = f32x4_t{};
@@ -459,7 +466,7 @@ __global__ void __launch_bounds__(BLK * 2)
 #pragma unroll
       for (int st = 0; st < 2; ++st) pb[a2][st] = bf16x8_t{};
     wait_vm_barrier<0>();
-    mfma_pair<D, BLK, true, false>(ka, 0, qreg, sc[0], va, 0, pb[1], oacc);
+    mfma_pair<D, BLK, BK, true, false>(ka, 0, qreg, sc[0], va, 0, pb[1], oacc);
 
     // Sub-iteration s = R*u + H (H static).  On entry the raw scores of s are
     // in sc[H & 1] and the probabilities of s-1 in pb[(H + 1) & 1].  The
@@ -489,17 +496,18 @@ __global__ void __launch_bounds__(BLK * 2)
       auto issue = [&](int t) {
         if (t < C::LPW) {
           dma16(lds0 + H * C::SUB + (w * C::LPW + t) * 1024, krs, koffs[t],
-                (uint32_t)((jk * BLK + (H % NS) * 32) * C::KROW));
+                (uint32_t)((jk * BK + (H % NS) * 32) * C::KROW));
         } else {
           const int u = t - C::LPW;
           dma16(lds0 + C::RING + (HV % R) * C::SUB + (w * C::LPW + u) * 1024, vrs, voff0 + u * 1024,
                 (uint32_t)((jv * NS + HV % NS) * C::SUB));
         }
       };
-      // ragged last key block: mask the keys >= N of this sub-tile
-      const int kvb = N - jc[H / NS] * BLK;
+      // ragged last key block: mask the keys >= N of this sub-tile; a
+      // padding sub-tile past the real stream is masked whole
+      const int kvb = (R * u + H < S_real) ? N - jc[H / NS] * BK : 0;
       if (kvb < (H % NS + 1) * 32) mask_sub(cur, H % NS, kvb, g);
-      float ls = pipeline_step<D, BLK, 4, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
+      float ls = pipeline_step<D, BLK, BK, 4, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
                                           ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc,
                                           cur, scale_log2, m_run, pb[H & 1], issue);
       // The probabilities of s were taken against the running max without
@@ -553,7 +561,7 @@ __global__ void __launch_bounds__(BLK * 2)
     // the workgroup's LDS can be handed to another workgroup
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     // drain: P V of the last sub-tile S-1 (odd, so its probabilities are pb[1])
-    mfma_pair<D, BLK, false, true>(ka, 0, qreg, sc[0], va, (uint32_t)(((S - 1) % R) * C::SUB),
+    mfma_pair<D, BLK, BK, false, true>(ka, 0, qreg, sc[0], va, (uint32_t)(((S - 1) % R) * C::SUB),
                                    pb[1], oacc);
   }
 
@@ -664,13 +672,13 @@ __global__ void __launch_bounds__(256)
 // per row) at the next 256-byte boundary.
 size_t vt_bytes(int BH, int n_pad, int d) { return ((size_t)BH * n_pad * d * 2 + 255) / 256 * 256; }
 
-template <int D, int BLK>
+template <int D, int BLK, int BK>
 hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H, int N, int n_pad,
                       float scale, const int32_t* row_ptr, const int32_t* col_idx,
                       int64_t col_len, void* o, float* lse, void* workspace, hipStream_t stream) {
   const int BH = B * H;
   const int n_q = n_pad / BLK;
-  const int n_k = n_pad / BLK;
+  const int n_k = n_pad / BK;
   const int rows = BH * n_q;
   __bf16* vt = static_cast<__bf16*>(workspace);
   int* order = reinterpret_cast<int*>(static_cast<char*>(workspace) + vt_bytes(BH, n_pad, D));
@@ -680,7 +688,7 @@ hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H,
   dim3 tgrid(n_pad / 64, BH);
   hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
                      static_cast<const __bf16*>(v), vt, n_pad);
-  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK>), dim3(rows), dim3(FwdCfg<D, BLK>::NT), 0,
+  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(FwdCfg<D, BLK, BK>::NT), 0,
                      stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(vt), row_ptr, col_idx, col_len,
                      static_cast<__bf16*>(o), lse, order, n_q, n_k, N, n_pad, scale * kLog2e);
@@ -689,23 +697,24 @@ hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H,
 
 }  // namespace
 
-hipError_t launch_sparse_fwd_bf16(int d, int blk, const void* q, const void* k, const void* v,
-                                  int B, int H, int N, int n_pad, float scale,
+hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, const void* k,
+                                  const void* v, int B, int H, int N, int n_pad, float scale,
                                   const int32_t* row_ptr, const int32_t* col_idx,
                                   int64_t col_len, void* o, float* lse, void* workspace,
                                   hipStream_t stream) {
-  if (d == 128 && blk == 128)
-    return launch_fwd<128, 128>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o,
-                                lse, workspace, stream);
-  if (d == 64 && blk == 128)
-    return launch_fwd<64, 128>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, lse,
-                               workspace, stream);
-  if (d == 128 && blk == 64)
-    return launch_fwd<128, 64>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, lse,
-                               workspace, stream);
-  if (d == 64 && blk == 64)
-    return launch_fwd<64, 64>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, lse,
-                              workspace, stream);
+#define LOSA_FWD(DD, BB, KK)                                                                 \
+  if (d == DD && blk == BB && blk_k == KK)                                                   \
+    return launch_fwd<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, \
+                                  o, lse, workspace, stream);
+  LOSA_FWD(128, 128, 128)
+  LOSA_FWD(64, 128, 128)
+  LOSA_FWD(128, 64, 64)
+  LOSA_FWD(64, 64, 64)
+  LOSA_FWD(128, 128, 32)
+  LOSA_FWD(64, 128, 32)
+  LOSA_FWD(128, 64, 32)
+  LOSA_FWD(64, 64, 32)
+#undef LOSA_FWD
   return hipErrorInvalidValue;
 }
 

@@ -50,6 +50,7 @@ class Workload:
     sigma: float          # per-step drift std
     reuse: int            # reuse steps after the calibration step
     seed: int
+    block_k: int = 0      # key block C when it differs from the query block (0: C = R)
 
     @property
     def N(self) -> int:
@@ -62,7 +63,18 @@ class Workload:
 
     @property
     def n_blocks(self) -> int:
+        """Query blocks per head (n_q)."""
         return self.N_pad // self.block
+
+    @property
+    def bk(self) -> int:
+        """Key block size C."""
+        return self.block_k or self.block
+
+    @property
+    def n_kblocks(self) -> int:
+        """Key blocks per head (n_k)."""
+        return self.N_pad // self.bk
 
     @property
     def torch_dtype(self):
@@ -98,9 +110,16 @@ def sweep_points():
             for a in SWEEP_ALPHAS for t in SWEEP_TAUS]
 
 
-def scaled(w: Workload, grid=None, H=None, B=None, name=None) -> Workload:
+def scaled(w: Workload, grid=None, H=None, B=None, name=None, block_k=None) -> Workload:
     """The same construction at a smaller grid / head count (parity cases)."""
-    return replace(w, grid=grid or w.grid, H=H or w.H, B=B or w.B, name=name or w.name)
+    return replace(w, grid=grid or w.grid, H=H or w.H, B=B or w.B, name=name or w.name,
+                   block_k=w.block_k if block_k is None else block_k)
+
+
+def rectangular(w: Workload, block_k: int = 32) -> Workload:
+    """The same inputs with the paper's rectangular blocks: query blocks of
+    w.block rows, key blocks of block_k keys (Sec. 5.1 uses 128 x 32)."""
+    return replace(w, block_k=block_k, name=f"{w.name}-c{block_k}")
 
 
 def _gen(device, seed: int) -> torch.Generator:

@@ -75,20 +75,21 @@ def sample_rows(w, extra=()):
 
 def run_case(L, w, tau, reuse=0, rows=None, label=""):
     """calibrate -> select -> sparse fwd (+ reuse steps), all checked against the oracle."""
-    N, C, scale = w.N, w.block, w.scale
-    n_q = w.n_blocks
-    n_kv = O.num_valid_key_blocks(N, C)
+    N, Cq, Ck, scale = w.N, w.block, w.bk, w.scale
+    n_q, n_k = w.n_blocks, w.n_kblocks
+    n_kv = O.num_valid_key_blocks(N, Ck)
     t32 = tau32(tau)
-    say(f"{label}: generate {w.name} B={w.B} H={w.H} N={N} d={w.d} block={C} {w.dtype} tau={tau}")
+    say(f"{label}: generate {w.name} B={w.B} H={w.H} N={N} d={w.d} blocks={Cq}x{Ck} {w.dtype} "
+        f"tau={tau}")
     state = W.make_state(w, device="cuda")
     q, k, v = W.cast(state, w)
 
     say(f"{label}: calibrate")
-    mass, lse = L.losa_calibrate_mass(q, k, N, C)
+    mass, lse = L.losa_calibrate_mass(q, k, N, Cq, Ck)
     say(f"{label}: select")
-    rp, ci = L.losa_select_blocks(mass, N, C, C, tau)
+    rp, ci = L.losa_select_blocks(mass, N, Cq, Ck, tau)
     say(f"{label}: sparse fwd step 0")
-    o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, C, C, rp, ci, want_lse=True)
+    o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, Cq, Ck, rp, ci, want_lse=True)
     torch.cuda.synchronize()
     say(f"{label}: oracle")
 
@@ -98,30 +99,30 @@ def run_case(L, w, tau, reuse=0, rows=None, label=""):
     nnz = int(rp_g[-1])
     ci_g = ci[:nnz].cpu().numpy().astype(np.int64)
     R = w.B * w.H * n_q
-    assert O.validate_csr(rp_g, ci_g, R, n_q, N, C, n_q) == []
+    assert O.validate_csr(rp_g, ci_g, R, n_k, N, Cq, n_q) == []
 
     # properties at any size: every row of masses sums to one; recall >= tau
-    sums = mass_g.reshape(R, n_q).sum(axis=1)
+    sums = mass_g.reshape(R, n_k).sum(axis=1)
     assert np.all(np.abs(sums - 1.0) < 1e-4), f"mass rows sum to {sums.min()}..{sums.max()}"
     if t32 < 1:
-        assert O.recall(mass_g, rp_g, ci_g, N, C) >= t32 - 1e-5
+        assert O.recall(mass_g, rp_g, ci_g, N, Cq) >= t32 - 1e-5
     else:
         assert nnz == R * n_kv
 
     todo = list(range(R)) if rows is None else rows
-    m_ref, l_ref = O.block_masses(qh, kh, N, C, C, scale, rows_subset=todo)
-    flat_m_ref = m_ref.reshape(R, n_q)
-    flat_m_g = mass_g.reshape(R, n_q)
+    m_ref, l_ref = O.block_masses(qh, kh, N, Cq, Ck, scale, rows_subset=todo)
+    flat_m_ref = m_ref.reshape(R, n_k)
+    flat_m_g = mass_g.reshape(R, n_k)
     merr = np.abs(flat_m_g[todo] - flat_m_ref[todo]).max()
     say(f"{label}: mass max-abs err {merr:.3e}")
     assert merr <= MASS_TOL
-    qrows = np.concatenate([np.arange(i * C, min((i + 1) * C, N)) + (r // n_q) * w.N_pad
+    qrows = np.concatenate([np.arange(i * Cq, min((i + 1) * Cq, N)) + (r // n_q) * w.N_pad
                             for r in todo for i in [r % n_q]])
     lerr = np.abs(lse_g.reshape(-1)[qrows] - l_ref.reshape(-1)[qrows]).max()
     assert lerr <= LSE_TOL, f"lse err {lerr}"
 
     # selection: the GPU's rows against the oracle's selection on oracle masses
-    details = [O.select_row(flat_m_ref[r], t32, n_kv, (r % n_q) * C < N) for r in todo]
+    details = [O.select_row(flat_m_ref[r], t32, n_kv, (r % n_q) * Cq < N) for r in todo]
     srp, sci = sub_csr(rp_g, ci_g, todo)
     cmp = CMP.compare_selection(srp, sci, details, flat_m_ref[todo], t32)
     say(f"{label}: selection {cmp}")
@@ -134,10 +135,10 @@ def run_case(L, w, tau, reuse=0, rows=None, label=""):
             W.drift_(state, w, step)
             q, k, v = W.cast(state, w)
             say(f"{label}: sparse fwd reuse step {step}")
-            o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, C, C, rp, ci, want_lse=True)
+            o, lse_o = L.losa_sparse_attn_fwd(q, k, v, N, Cq, Ck, rp, ci, want_lse=True)
             torch.cuda.synchronize()
             qh, kh, vh = f64(q), f64(k), f64(v)
-        o_ref, lo_ref = O.sparse_attention(qh, kh, vh, N, C, C, scale, rp_g, ci_g,
+        o_ref, lo_ref = O.sparse_attention(qh, kh, vh, N, Cq, Ck, scale, rp_g, ci_g,
                                            rows_subset=todo)
         og = f64(o)
         err = np.abs(og.reshape(-1, w.d)[qrows] - o_ref.reshape(-1, w.d)[qrows])
@@ -149,7 +150,7 @@ def run_case(L, w, tau, reuse=0, rows=None, label=""):
         og4 = og.reshape(w.B, w.H, w.N_pad, w.d)
         assert np.all(og4[:, :, N:] == 0)
         assert np.all(np.isneginf(f64(lse_o)[:, :, N:]))
-    return dict(nnz=nnz, coverage=nnz / (R * n_q), exempt=cmp["exempt"])
+    return dict(nnz=nnz, coverage=nnz / (R * n_k), exempt=cmp["exempt"])
 
 
 # ----------------------------------------------------------------------------
@@ -168,6 +169,16 @@ SMALL = {
                                   0.5, 0.02, 1, 79),
     "f32-d64-blk128": W.Workload("f32-d64-b128", 1, 3, 64, "f32", (2, 10, 19), 128, 0.9, 1.5,
                                  0.5, 0.02, 1, 80),
+    # the paper's rectangular blocks (Sec. 5.1): 128-row query blocks, 32-key key blocks
+    "wan-bf16-d128-r128c32": W.rectangular(W.scaled(W.WORKLOADS["wan"], grid=(4, 12, 30), H=3,
+                                                    name="wan-small")),
+    "cog-bf16-d64-r128c32": W.rectangular(W.scaled(W.WORKLOADS["cog"], grid=(3, 10, 45), H=4,
+                                                   name="cog-small")),
+    "bf16-d128-r64c32": W.rectangular(W.Workload("b64", 1, 2, 128, "bf16", (3, 9, 25), 64, 0.99,
+                                                 1.5, 0.5, 0.02, 1, 81)),
+    "tiny-f32-r64c32": W.rectangular(W.WORKLOADS["tiny"]),
+    "f32-d128-r128c32": W.rectangular(W.Workload("f32-d128-b128", 1, 2, 128, "f32", (2, 10, 25),
+                                                 128, 0.99, 1.5, 0.5, 0.02, 1, 82)),
 }
 
 
@@ -178,39 +189,41 @@ def test_small_pipeline_all_rows(L, key):
     assert 0 < info["coverage"] <= 1
 
 
-@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32"])
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32",
+                                 "wan-bf16-d128-r128c32", "tiny-f32-r64c32"])
 def test_small_tau_one_is_dense(L, key):
     w = SMALL[key]
     q, k, v = W.make_inputs(w, device="cuda")
-    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, want_lse=False)
-    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, 1.0)
-    o = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci)
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk, want_lse=False)
+    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.bk, 1.0)
+    o = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk, rp, ci)
     torch.cuda.synchronize()
-    assert L.nnz(rp) == w.B * w.H * w.n_blocks * w.n_blocks
+    assert L.nnz(rp) == w.B * w.H * w.n_blocks * O.num_valid_key_blocks(w.N, w.bk)
     o_ref, _ = O.dense_attention(f64(q), f64(k), f64(v), w.N, w.scale)
     mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
     tmax, tmean = out_tol(w)
     assert mx <= tmax and mean <= tmean, (mx, mean)
 
 
-@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32"])
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "cog-bf16-d64-ragged", "tiny-f32",
+                                 "wan-bf16-d128-r128c32"])
 def test_select_on_oracle_masses(L, key):
     # the selection kernel alone, fed the oracle's masses (rounded to fp32 for
     # both sides), at several thresholds
     w = SMALL[key]
     q, k, _ = W.make_inputs(w)
-    m_ref, _ = O.block_masses(q.float().numpy(), k.float().numpy(), w.N, w.block, w.block, w.scale)
+    m_ref, _ = O.block_masses(q.float().numpy(), k.float().numpy(), w.N, w.block, w.bk, w.scale)
     m32 = m_ref.astype(np.float32)
     mdev = torch.from_numpy(m32).cuda()
-    n_q = w.n_blocks
-    n_kv = O.num_valid_key_blocks(w.N, w.block)
+    n_k = w.n_kblocks
+    n_kv = O.num_valid_key_blocks(w.N, w.bk)
     for tau in (0.5, 0.9, 0.95, 0.99, 0.999, 1.0):
-        rp, ci = L.losa_select_blocks(mdev, w.N, w.block, w.block, tau)
+        rp, ci = L.losa_select_blocks(mdev, w.N, w.block, w.bk, tau)
         torch.cuda.synchronize()
         rp_g = rp.cpu().numpy().astype(np.int64)
         ci_g = ci[:rp_g[-1]].cpu().numpy().astype(np.int64)
         m64 = m32.astype(np.float64)
-        details = [O.select_row(m64.reshape(-1, n_q)[r], tau32(tau), n_kv) for r in range(rp_g.size - 1)]
+        details = [O.select_row(m64.reshape(-1, n_k)[r], tau32(tau), n_kv) for r in range(rp_g.size - 1)]
         cmp = CMP.compare_selection(rp_g, ci_g, details, m64, tau32(tau))
         assert cmp["ok"], (tau, cmp)
 
@@ -226,11 +239,14 @@ def test_select_ties_go_to_smaller_index(L):
     assert ci[:rp_h[-1]].cpu().numpy().reshape(-1, 4).tolist() == [[0, 1, 2, 3]] * (B * H * n)
 
 
-def test_fwd_edge_case_csr(L):
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "wan-bf16-d128-r128c32"])
+def test_fwd_edge_case_csr(L, key):
     # empty row, single-block row, descending order, out-of-range ids, full row
-    w = SMALL["wan-bf16-d128-ragged"]
+    # (with 32-key blocks the row lengths 1, 3, 2 and n_k also cover every
+    # remainder of the stream padding to whole loop passes)
+    w = SMALL[key]
     q, k, v = W.make_inputs(w, device="cuda")
-    n_q = n_k = w.n_blocks
+    n_q, n_k = w.n_blocks, w.n_kblocks
     R = w.B * w.H * n_q
     rows = []
     for r in range(R):
@@ -251,12 +267,12 @@ def test_fwd_edge_case_csr(L):
     ci = np.array([j for seg in rows for j in seg], np.int64)
     rp_d = torch.from_numpy(rp.astype(np.int32)).cuda()
     ci_d = torch.from_numpy(ci.astype(np.int32)).cuda()
-    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp_d, ci_d, want_lse=True)
+    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk, rp_d, ci_d, want_lse=True)
     torch.cuda.synchronize()
     # ids outside [0, n_k) are ignored by contract: drop them for the oracle
     keep = (ci >= 0) & (ci < n_k)
     rp_clean = np.concatenate([[0], np.cumsum([np.sum(keep[rp[r]:rp[r + 1]]) for r in range(R)])])
-    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.bk, w.scale,
                                       rp_clean, ci[keep])
     mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
     assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
@@ -271,26 +287,27 @@ def test_fwd_edge_case_csr(L):
 
     # a col_idx shorter than row_ptr claims: row bounds are clamped
     cut = int(rp[-1]) - 7
-    o2 = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp_d, ci_d[:cut])
+    o2 = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk, rp_d, ci_d[:cut])
     torch.cuda.synchronize()
     rp_cut = np.minimum(rp, cut)
     ci_cut = ci[:cut]
     keep = (ci_cut >= 0) & (ci_cut < n_k)
     rp_cut_clean = np.concatenate([[0], np.cumsum([np.sum(keep[rp_cut[r]:rp_cut[r + 1]])
                                                    for r in range(R)])])
-    o_ref2, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+    o_ref2, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.bk, w.scale,
                                    rp_cut_clean, ci_cut[keep])
     mx, mean = CMP.output_errors(f64(o2), o_ref2, w.N)
     assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
 
 
-@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "f32-d128-blk128"])
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "f32-d128-blk128",
+                                 "bf16-d128-r64c32", "f32-d128-r128c32"])
 def test_fwd_repeated_ids_count_once(L, key):
     # K(q) of Eq. (4) is a set: an id listed twice (or more) must weigh its
     # keys once, exactly as the deduplicated row
     w = SMALL[key]
     q, k, v = W.make_inputs(w, device="cuda")
-    n_q = n_k = w.n_blocks
+    n_q, n_k = w.n_blocks, w.n_kblocks
     R = w.B * w.H * n_q
     rng = np.random.default_rng(1234)
     rows, clean = [], []
@@ -306,11 +323,11 @@ def test_fwd_repeated_ids_count_once(L, key):
     rp_c = np.concatenate([[0], np.cumsum([len(x) for x in clean])]).astype(np.int64)
     ci_c = np.concatenate(clean).astype(np.int64)
     say(f"repeated ids {key}: {R} rows, {ci.size} entries, {ci_c.size} distinct")
-    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block,
+    o, lse = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk,
                                     torch.from_numpy(rp.astype(np.int32)).cuda(),
                                     torch.from_numpy(ci.astype(np.int32)).cuda(), want_lse=True)
     torch.cuda.synchronize()
-    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.bk, w.scale,
                                       rp_c, ci_c)
     tmax, tmean = out_tol(w)
     mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
@@ -319,7 +336,8 @@ def test_fwd_repeated_ids_count_once(L, key):
     assert np.abs(f64(lse)[valid] - l_ref[valid]).max() <= LSE_TOL
 
 
-@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "cog-bf16-d64-ragged"])
+@pytest.mark.parametrize("key", ["wan-bf16-d128-ragged", "bf16-d64-blk64", "cog-bf16-d64-ragged",
+                                 "cog-bf16-d64-r128c32"])
 def test_fwd_writes_every_row_once(L, key):
     # the forward dispatches rows in a computed order (per-XCD, longest
     # first): every row of O and lse must be written, with the row count not
@@ -328,15 +346,15 @@ def test_fwd_writes_every_row_once(L, key):
     q, k, v = W.make_inputs(w, device="cuda")
     R = w.B * w.H * w.n_blocks
     say(f"every row {key}: {R} rows")
-    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block)
-    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, w.tau)
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk)
+    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.bk, w.tau)
     o = torch.full_like(q, float("nan"))
     lse = torch.full((w.B, w.H, w.N_pad), float("nan"), dtype=torch.float32, device=q.device)
-    L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci, want_lse=True, out=o, lse=lse)
+    L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk, rp, ci, want_lse=True, out=o, lse=lse)
     torch.cuda.synchronize()
     assert not torch.isnan(o).any().item()
     assert not torch.isnan(lse).any().item()
-    o_ref, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.block, w.scale,
+    o_ref, _ = O.sparse_attention(f64(q), f64(k), f64(v), w.N, w.block, w.bk, w.scale,
                                   rp.cpu().numpy().astype(np.int64),
                                   ci[:L.nnz(rp)].cpu().numpy().astype(np.int64))
     mx, mean = CMP.output_errors(f64(o), o_ref, w.N)
@@ -361,9 +379,9 @@ def test_deterministic(L):
 # full-size workloads, sampled rows
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan"])
+@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32", "hunyuan-c32"])
 def test_full_size_sampled(L, key):
-    w = W.WORKLOADS[key]
+    w = (W.rectangular(W.WORKLOADS[key[:-4]]) if key.endswith("-c32") else W.WORKLOADS[key])
     info = run_case(L, w, w.tau, reuse=1, rows=sample_rows(w), label=f"full-{key}")
     say(f"full-{key}: coverage {info['coverage']:.3f} nnz {info['nnz']}")
 
