@@ -13,6 +13,8 @@ reordering beyond what the definition states:
 * Recall(Omega) and Coverage(Omega)                           -- Sec. 3.1, Eq. (2)
 * mass-ordered shortest prefix s and the set Omega            -- Sec. 4.1, Eq. (3)
 * frozen-support (block-sparse) attention                     -- Sec. 4.2, Eq. (4)
+* the fixed-ratio top-k rule of the selection ablation        -- Sec. 5, Table 2
+* recall of a frozen support per query block and per head     -- Sec. 3.1, Eq. (2)
 
 Readings taken where the paper is silent (each is also what the GPU path does):
 
@@ -215,6 +217,37 @@ def select_blocks(mbar, N: int, block_q: int, block_k: int, tau: float):
     return row_ptr, col_idx.astype(np.int64), details
 
 
+def select_row_topk(mrow, k: int, n_k_valid: int, has_valid_rows: bool = True) -> RowSelection:
+    """Fixed-ratio top-k rule (the ablation of Table 2): the k largest masses of
+    the row in the same order as Eq. (3)'s (ties: smaller index first), k
+    clamped to the blocks that hold a valid key.  Padding-only blocks carry no
+    mass and have the largest indices, so they never enter while k <= n_k_valid."""
+    mrow = np.asarray(mrow, dtype=np.float64)
+    order = mass_order(mrow)
+    cum = np.cumsum(mrow[order])
+    s = min(int(k), n_k_valid) if has_valid_rows else 0
+    return RowSelection(order=order, cum=cum, s=s, omega=np.sort(order[:s]).astype(np.int64))
+
+
+def select_blocks_topk(mbar, N: int, block_q: int, block_k: int, k: int):
+    """The top-k rule on every (b, h, i) row, emitted as CSR like select_blocks."""
+    mbar = np.asarray(mbar, dtype=np.float64)
+    B, H, n_q, n_k = mbar.shape
+    nkv = num_valid_key_blocks(N, block_k)
+    rows = B * H * n_q
+    row_ptr = np.zeros(rows + 1, dtype=np.int64)
+    cols, details = [], []
+    for r in range(rows):
+        b, rem = divmod(r, H * n_q)
+        h, i = divmod(rem, n_q)
+        sel = select_row_topk(mbar[b, h, i], k, nkv, i * block_q < N)
+        details.append(sel)
+        cols.append(sel.omega)
+        row_ptr[r + 1] = row_ptr[r] + sel.omega.size
+    col_idx = np.concatenate(cols) if cols else np.zeros(0, dtype=np.int64)
+    return row_ptr, col_idx.astype(np.int64), details
+
+
 def validate_csr(row_ptr, col_idx, rows: int, n_k: int, N: int | None = None,
                  block_q: int | None = None, n_q: int | None = None) -> list[str]:
     """Structural checks of a CSR block list; returns the problems found."""
@@ -327,6 +360,35 @@ def coverage(row_ptr, B: int, H: int, n_q: int, n_k: int) -> float:
     """Coverage = mean over heads of sum_i |Omega_i| / (n_q n_k)."""
     nnz = int(np.asarray(row_ptr)[-1])
     return nnz / float(B * H * n_q * n_k)
+
+
+def recall_rows(mbar, row_ptr, col_idx) -> np.ndarray:
+    """Per query block: the retained share of its mass, sum over the distinct
+    ids of Omega_r inside [0, n_k) of mbar(r, j).  Masses of a query block sum
+    to one, so this is Eq. (2) restricted to that block."""
+    mbar = np.asarray(mbar, dtype=np.float64)
+    n_k = mbar.shape[-1]
+    flat = mbar.reshape(-1, n_k)
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    col_idx = np.asarray(col_idx, dtype=np.int64)
+    out = np.zeros(flat.shape[0])
+    for r in range(flat.shape[0]):
+        js = np.unique(col_idx[row_ptr[r]:row_ptr[r + 1]])
+        js = js[(js >= 0) & (js < n_k)]
+        out[r] = flat[r, js].sum()
+    return out
+
+
+def recall_heads(mbar, row_ptr, col_idx, N: int, block_q: int) -> np.ndarray:
+    """Eq. (2) per (b, h): sum_i sum_{j in Omega_i} M(i, j) / sum_i sum_j M(i, j)
+    with M(i, j) = R_i * mbar(i, j), R_i the valid rows of query block i
+    (so the denominator is N).  Returns [B, H]."""
+    mbar = np.asarray(mbar, dtype=np.float64)
+    B, H, n_q, n_k = mbar.shape
+    Ri = np.array([valid_rows(i, block_q, N).size for i in range(n_q)], dtype=np.float64)
+    rec = recall_rows(mbar, row_ptr, col_idx).reshape(B, H, n_q)
+    tot = (mbar * Ri[None, None, :, None]).sum(axis=(2, 3))
+    return (rec * Ri[None, None, :]).sum(axis=2) / tot
 
 
 def recall(mbar, row_ptr, col_idx, N: int, block_q: int) -> float:

@@ -274,6 +274,130 @@ def test_padding_only_blocks_are_never_kept():
 
 
 # ----------------------------------------------------------------------------
+# the fixed-ratio top-k rule (Table 2): brute force, link to Eq. (3), nesting
+# ----------------------------------------------------------------------------
+
+def check_topk_brute_force(seed=15, trials=40) -> bool:
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        n_k = int(rng.integers(1, 10))
+        m = rng.random(n_k) ** 2
+        if t % 2 == 0:                  # force ties
+            m = np.round(m * 3) / 3 + 0.02
+        m = m / m.sum()
+        for k in range(1, n_k + 1):
+            sel = O.select_row_topk(m, k, n_k)
+            if sel.s != k or sel.omega.size != k:
+                return False
+            best = max(m[list(c)].sum() for c in itertools.combinations(range(n_k), k))
+            if abs(m[sel.omega].sum() - best) > 1e-15:
+                return False
+            thr = m[sel.order[k - 1]]
+            strictly = set(np.nonzero(m > thr)[0].tolist())
+            ties = sorted(np.nonzero(m == thr)[0].tolist())
+            if sel.omega.tolist() != sorted(strictly | set(ties[:k - len(strictly)])):
+                return False
+    return True
+
+
+def test_topk_is_the_heaviest_k_subset_brute_force():
+    assert check_topk_brute_force()
+
+
+def test_topk_at_the_prefix_length_equals_the_threshold_rule():
+    # both rules walk the same mass order: keeping the s of Eq. (3) blocks is
+    # the threshold selection itself
+    rng = np.random.default_rng(16)
+    N, Np, d, R, C = 61, 64, 8, 8, 4
+    q, k, _ = _rand_qkv(rng, N=N, Np=Np, d=d, scale_qk=1.3)
+    mbar, _ = O.block_masses(q, k, N, R, C, 1 / math.sqrt(d))
+    nkv = O.num_valid_key_blocks(N, C)
+    for tau in (0.5, 0.9, 0.99):
+        for row in mbar.reshape(-1, Np // C):
+            sel = O.select_row(row, tau, nkv)
+            assert O.select_row_topk(row, sel.s, nkv).omega.tolist() == sel.omega.tolist()
+
+
+def test_topk_nested_clamped_and_padding_free():
+    rng = np.random.default_rng(17)
+    N, Np, d, R, C = 50, 64, 8, 16, 4   # key blocks 13..15 hold only padding
+    q, k, _ = _rand_qkv(rng, N=N, Np=Np, d=d)
+    mbar, _ = O.block_masses(q, k, N, R, C, 0.4)
+    nkv = O.num_valid_key_blocks(N, C)
+    prev = None
+    for kk in range(1, Np // C + 3):
+        rp, ci, _ = O.select_blocks_topk(mbar, N, R, C, kk)
+        assert O.validate_csr(rp, ci, 2 * (Np // R), Np // C, N, R, Np // R) == []
+        assert np.all(np.diff(rp) == min(kk, nkv))
+        assert ci.max() < nkv
+        sets = [set(ci[rp[r]:rp[r + 1]].tolist()) for r in range(len(rp) - 1)]
+        if prev is not None:
+            assert all(a <= b for a, b in zip(prev, sets))
+        prev = sets
+    assert all(st == set(range(nkv)) for st in prev)
+
+
+# ----------------------------------------------------------------------------
+# recall of a frozen support (Eq. (2)) per query block and per head
+# ----------------------------------------------------------------------------
+
+def check_recall_closed_form(seed=18) -> bool:
+    # K = 0: every valid key gets probability 1/N, so M(i, j) = R_i |B_j ∩ [0,N)| / N
+    # and a support's recall is the count of its distinct valid keys over N,
+    # per query block and per head, exactly (duplicates and stray ids ignored)
+    rng = np.random.default_rng(seed)
+    N, Np, d, R, C = 45, 48, 4, 16, 8   # ragged last query and key block
+    q, k, _ = _rand_qkv(rng, N=N, Np=Np, d=d)
+    k[:] = 0.0
+    mbar, _ = O.block_masses(q, k, N, R, C, 1.0)
+    n_q, n_k = Np // R, Np // C
+    rows, want = [], []
+    for r in range(2 * n_q):
+        js = rng.choice(n_k, size=int(rng.integers(1, n_k + 1)), replace=True)
+        rows.append(np.concatenate([js, [-1, n_k + 2]]))
+        want.append(sum(min(C, N - j * C) for j in set(js.tolist())) / N)
+    rp = np.concatenate([[0], np.cumsum([len(x) for x in rows])])
+    ci = np.concatenate(rows)
+    got = O.recall_rows(mbar, rp, ci)
+    if not np.allclose(got, want, rtol=0, atol=1e-12):
+        return False
+    Ri = np.array([min(R, N - i * R) for i in range(n_q)], dtype=float)
+    heads = O.recall_heads(mbar, rp, ci, N, R)
+    want_h = [(np.array(want[h * n_q:(h + 1) * n_q]) * Ri).sum() / N for h in range(2)]
+    return bool(np.allclose(heads[0], want_h, rtol=0, atol=1e-12))
+
+
+def test_recall_closed_form_uniform_attention():
+    assert check_recall_closed_form()
+
+
+def test_recall_weights_query_blocks_by_their_valid_rows():
+    # two query blocks of one head, the second ragged with 1 valid row of 4:
+    # Eq. (2) weights block recall by rows, 4 * 1.0 + 1 * 0.0 over 5 rows
+    mbar = np.array([[[[0.5, 0.5], [0.25, 0.75]]]])
+    rp = np.array([0, 2, 2])
+    ci = np.array([0, 1])
+    assert O.recall_rows(mbar, rp, ci).tolist() == [1.0, 0.0]
+    assert O.recall_heads(mbar, rp, ci, 5, 4)[0, 0] == pytest.approx(0.8, abs=1e-15)
+    assert O.recall(mbar, rp, ci, 5, 4) == pytest.approx(0.8, abs=1e-15)
+
+
+def test_recall_full_support_one_and_at_least_tau_at_construction():
+    rng = np.random.default_rng(19)
+    N, Np, d, R, C = 61, 64, 8, 8, 4
+    q, k, _ = _rand_qkv(rng, N=N, Np=Np, d=d, scale_qk=1.3)
+    mbar, _ = O.block_masses(q, k, N, R, C, 1 / math.sqrt(d))
+    rp, ci, _ = O.select_blocks(mbar, N, R, C, 1.0)
+    assert np.allclose(O.recall_rows(mbar, rp, ci), 1.0, atol=1e-12)
+    for tau in (0.5, 0.9, 0.99):
+        rp, ci, _ = O.select_blocks(mbar, N, R, C, tau)
+        assert np.all(O.recall_rows(mbar, rp, ci) >= tau - 1e-12)
+        heads = O.recall_heads(mbar, rp, ci, N, R)
+        assert np.all(heads >= tau - 1e-12)
+        assert heads.mean() == pytest.approx(O.recall(mbar, rp, ci, N, R), abs=1e-12)
+
+
+# ----------------------------------------------------------------------------
 # Eq. (4): token-level brute force, special cases, error bound
 # ----------------------------------------------------------------------------
 
@@ -413,13 +537,35 @@ def _masses_include_padding(q, k, N, R, C, scale):
     return _orig_masses(q, k, Np, R, C, scale)
 
 
+def _recall_rows_counts_duplicates(mbar, row_ptr, col_idx):
+    mbar = np.asarray(mbar, dtype=np.float64)
+    n_k = mbar.shape[-1]
+    flat = mbar.reshape(-1, n_k)
+    out = np.zeros(flat.shape[0])
+    for r in range(flat.shape[0]):
+        js = np.asarray(col_idx[row_ptr[r]:row_ptr[r + 1]])
+        out[r] = flat[r, js[(js >= 0) & (js < n_k)]].sum()
+    return out
+
+
+def _recall_heads_unweighted(mbar, row_ptr, col_idx, N, block_q):
+    B, H, n_q, _ = np.asarray(mbar).shape
+    return O.recall_rows(mbar, row_ptr, col_idx).reshape(B, H, n_q).mean(axis=2)
+
+
+def _topk_off_by_one(mrow, k, n_k_valid, has_valid_rows=True):
+    return _orig_topk(mrow, max(k - 1, 0), n_k_valid, has_valid_rows)
+
+
 _orig_sparse = O.sparse_attention
 _orig_masses = O.block_masses
 _orig_select_row = O.select_row
+_orig_topk = O.select_row_topk
 
 ALL_PINS = [check_golden, check_dense_vs_sdpa, check_sparse_full_equals_dense,
             check_masses_brute_force, check_selection_brute_force,
-            check_token_mask_equals_blockwise]
+            check_token_mask_equals_blockwise, check_topk_brute_force,
+            check_recall_closed_form]
 
 
 def _some_pin_fails():
@@ -442,6 +588,9 @@ def _some_pin_fails():
     ("sparse_attention", _sparse_no_scale),
     ("block_masses", _masses_sum_not_mean),
     ("block_masses", _masses_include_padding),
+    ("select_row_topk", _topk_off_by_one),
+    ("recall_rows", _recall_rows_counts_duplicates),
+    ("recall_heads", _recall_heads_unweighted),
 ])
 def test_planted_mistake_is_caught(monkeypatch, attr, mutant):
     assert not _some_pin_fails(), "pins must hold for the unmodified oracle"
