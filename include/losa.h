@@ -106,6 +106,48 @@ losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block
                                void* stream);
 
 /*
+ * Fixed-ratio top-k selection: the rule the paper's selection ablation
+ * compares against (Sec. 5, Table 2), a uniform budget of k key blocks per
+ * query block instead of a retained-mass threshold.
+ *
+ * For each row r: the same order as losa_select_blocks (decreasing mass, ties
+ * by the smaller block index); keep its first min(k, n_kv) blocks, n_kv the
+ * key blocks holding a valid key.  Rows of query blocks with no valid query
+ * are empty.  Arguments, CSR output, capacity and workspace exactly as for
+ * losa_select_blocks (workspace: losa_workspace_bytes(1, ...)).  k < 1
+ * returns LOSA_ERR_INVALID_SHAPE.  To match the coverage of a threshold
+ * selection (as Table 2 does), pass k = round(nnz / (B*H*n_q)).
+ */
+losa_status losa_select_blocks_topk(const float* mass, int B, int H, int N, int block_q,
+                                    int block_k, int k, int32_t* row_ptr, int32_t* col_idx,
+                                    int64_t col_idx_capacity, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/*
+ * Recall of a frozen support on the block masses of another step (Sec. 3.1,
+ * Eq. (2)): how much attention mass the support fixed at the construction
+ * step still captures later (the paper's frozen-pattern analysis, Sec. 3.3).
+ *
+ * mass          fp32 [B][H][n_q][n_k], e.g. losa_calibrate_mass of step t.
+ * row_ptr, col_idx, col_idx_len   the support, with the conventions of
+ *               losa_sparse_attn_fwd (ids in any order, a repeated id counts
+ *               once, ids outside [0, n_k) ignored, row bounds clamped to
+ *               [0, col_idx_len]).  n_k <= 4096.
+ * recall_rows   out, nullable, fp32 [B*H*n_q]: per row the sum of its distinct
+ *               retained masses (masses of a query block sum to one, so this is
+ *               Eq. (2) restricted to that block); 0 for empty rows.
+ * recall_heads  out, nullable, fp32 [B*H]: Eq. (2) per head,
+ *               sum_i R_i * kept_i / sum_i R_i * total_i, R_i = valid rows of
+ *               query block i, total_i = the row's mass sum.
+ * workspace     >= losa_workspace_bytes(3, ...) bytes (per-row fp64 sums).
+ * Sums are taken in fp64 in a fixed order: results are bitwise repeatable.
+ */
+losa_status losa_block_recall(const float* mass, int B, int H, int N, int block_q, int block_k,
+                              const int32_t* row_ptr, const int32_t* col_idx, int64_t col_idx_len,
+                              float* recall_rows, float* recall_heads, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
  * Frozen-support block-sparse attention (Sec. 4.2, Eq. (4)).
  *
  * For every valid query q of query block i in head (b, h):
@@ -140,9 +182,9 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
                                  size_t workspace_bytes, void* stream);
 
 /*
- * Workspace bytes needed by: which = 0 losa_calibrate_mass, 1 losa_select_blocks,
- * 2 losa_sparse_attn_fwd.  Returns 0 for invalid arguments (then the call
- * itself reports the error).
+ * Workspace bytes needed by: which = 0 losa_calibrate_mass, 1 losa_select_blocks
+ * and losa_select_blocks_topk, 2 losa_sparse_attn_fwd, 3 losa_block_recall.
+ * Returns 0 for invalid arguments (then the call itself reports the error).
  */
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
                             int block_k);

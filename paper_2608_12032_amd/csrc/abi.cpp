@@ -117,17 +117,21 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
       "losa_calibrate_mass");
 }
 
-losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block_q, int block_k,
-                               float tau, int32_t* row_ptr, int32_t* col_idx,
-                               int64_t col_idx_capacity, void* workspace, size_t workspace_bytes,
-                               void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks and launch shared by the threshold rule (topk = 0) and the
+// fixed-ratio top-k rule (topk > 0).
+losa_status select_common(const char* where, const float* mass, int B, int H, int N, int block_q,
+                          int block_k, float tau, int topk, int32_t* row_ptr, int32_t* col_idx,
+                          int64_t col_idx_capacity, void* workspace, size_t workspace_bytes,
+                          void* stream) {
   if (!mass || !row_ptr || !col_idx || !workspace)
     return fail(LOSA_ERR_NULL_POINTER, "mass, row_ptr, col_idx and workspace must be non-NULL");
   Shape s;
   losa_status st = check_shape(B, H, N, 1, block_q, block_k, &s);
   if (st != LOSA_OK) return st;
-  if (std::isnan(tau) || !(tau > 0.f) || tau > 1.f)
-    return fail(LOSA_ERR_INVALID_TAU, "tau=%g must be in (0, 1]", (double)tau);
   if (!aligned16(mass) || !aligned16(row_ptr) || !aligned16(col_idx) || !aligned16(workspace))
     return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
   if (s.n_k > losa::select_max_nk())
@@ -143,9 +147,60 @@ losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block
   const size_t need = losa::select_workspace_bytes((int)s.rows, s.n_k);
   if (workspace_bytes < need)
     return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
-  return hip_status(losa::launch_select(mass, B, H, N, block_q, block_k, tau, row_ptr, col_idx,
-                                        workspace, static_cast<hipStream_t>(stream)),
-                    "losa_select_blocks");
+  return hip_status(losa::launch_select(mass, B, H, N, block_q, block_k, tau, topk, row_ptr,
+                                        col_idx, workspace, static_cast<hipStream_t>(stream)),
+                    where);
+}
+
+}  // namespace
+
+extern "C" {
+
+losa_status losa_select_blocks(const float* mass, int B, int H, int N, int block_q, int block_k,
+                               float tau, int32_t* row_ptr, int32_t* col_idx,
+                               int64_t col_idx_capacity, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  if (std::isnan(tau) || !(tau > 0.f) || tau > 1.f)
+    return fail(LOSA_ERR_INVALID_TAU, "tau=%g must be in (0, 1]", (double)tau);
+  return select_common("losa_select_blocks", mass, B, H, N, block_q, block_k, tau, 0, row_ptr,
+                       col_idx, col_idx_capacity, workspace, workspace_bytes, stream);
+}
+
+losa_status losa_select_blocks_topk(const float* mass, int B, int H, int N, int block_q,
+                                    int block_k, int k, int32_t* row_ptr, int32_t* col_idx,
+                                    int64_t col_idx_capacity, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (k < 1) return fail(LOSA_ERR_INVALID_SHAPE, "k=%d must be >= 1", k);
+  return select_common("losa_select_blocks_topk", mass, B, H, N, block_q, block_k, 1.0f, k,
+                       row_ptr, col_idx, col_idx_capacity, workspace, workspace_bytes, stream);
+}
+
+losa_status losa_block_recall(const float* mass, int B, int H, int N, int block_q, int block_k,
+                              const int32_t* row_ptr, const int32_t* col_idx, int64_t col_idx_len,
+                              float* recall_rows, float* recall_heads, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (!mass || !row_ptr || !workspace)
+    return fail(LOSA_ERR_NULL_POINTER, "mass, row_ptr and workspace must be non-NULL");
+  if (col_idx_len < 0) return fail(LOSA_ERR_INVALID_SHAPE, "col_idx_len must be >= 0");
+  if (col_idx_len > 0 && !col_idx)
+    return fail(LOSA_ERR_NULL_POINTER, "col_idx is NULL but col_idx_len > 0");
+  Shape s;
+  losa_status st = check_shape(B, H, N, 1, block_q, block_k, &s);
+  if (st != LOSA_OK) return st;
+  if (!aligned16(mass) || !aligned16(row_ptr) || (col_idx && !aligned16(col_idx)) ||
+      !aligned16(workspace) || (recall_rows && !aligned16(recall_rows)) ||
+      (recall_heads && !aligned16(recall_heads)))
+    return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
+  if (s.n_k > losa::kSparseFwdMaxNk)
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per row exceeds %d", s.n_k,
+                losa::kSparseFwdMaxNk);
+  const size_t need = losa::recall_workspace_bytes((int)s.rows);
+  if (workspace_bytes < need)
+    return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
+  return hip_status(losa::launch_recall(mass, B, H, N, block_q, s.n_q, s.n_k, row_ptr, col_idx,
+                                        col_idx_len, recall_rows, recall_heads, workspace,
+                                        static_cast<hipStream_t>(stream)),
+                    "losa_block_recall");
 }
 
 losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
@@ -191,7 +246,8 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
                             int block_k) {
   Shape s;
-  if (check_shape(B, H, N, which == 1 ? 1 : d, block_q, block_k, &s) != LOSA_OK) return 0;
+  if (check_shape(B, H, N, (which == 1 || which == 3) ? 1 : d, block_q, block_k, &s) != LOSA_OK)
+    return 0;
   switch (which) {
     case 0:
       return 0;
@@ -199,6 +255,8 @@ size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, in
       return losa::select_workspace_bytes((int)s.rows, s.n_k);
     case 2:
       return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) : 0;
+    case 3:
+      return losa::recall_workspace_bytes((int)s.rows);
     default:
       return 0;
   }

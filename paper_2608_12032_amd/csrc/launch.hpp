@@ -24,8 +24,9 @@ hipError_t launch_calibrate_f32(int d, int blk, int blk_k, const void* q, const 
                                 hipStream_t stream);
 size_t calib_bf16_lds_bytes(int d, int blk, int n_k);
 
+// topk > 0: keep the topk heaviest blocks of each row instead of the prefix reaching tau
 hipError_t launch_select(const float* mass, int B, int H, int N, int block_q, int block_k,
-                         float tau, int32_t* row_ptr, int32_t* col_idx, void* workspace,
+                         float tau, int topk, int32_t* row_ptr, int32_t* col_idx, void* workspace,
                          hipStream_t stream);
 size_t select_workspace_bytes(int rows, int n_k);
 int select_max_nk();
@@ -40,6 +41,14 @@ hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
                                  void* o, float* lse, hipStream_t stream);
 size_t sparse_fwd_bf16_workspace(int B, int H, int n_pad, int d, int n_q);
+
+// Recall of a frozen support (Eq. (2)): per row the retained and the total
+// mass (fp64, in the workspace), then per head the row-weighted ratio.
+hipError_t launch_recall(const float* mass, int B, int H, int N, int block_q, int n_q, int n_k,
+                         const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
+                         float* recall_rows, float* recall_heads, void* workspace,
+                         hipStream_t stream);
+size_t recall_workspace_bytes(int rows);
 
 // Largest n_k (key blocks per head) the sparse forward kernels accept: each
 // workgroup keeps one flag per key block of its row in LDS.

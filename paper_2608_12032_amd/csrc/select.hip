@@ -8,9 +8,11 @@
 //                by the smaller block index.  A bitonic sort in LDS, then an
 //                fp64 inclusive scan of the sorted masses; the prefix length
 //                s is the first position whose cumulative mass reaches tau.
-//                tau >= 1 keeps every key block that holds a real key.  The
-//                kept blocks are flagged in a per-row byte mask and s is
-//                stored as the row's count.
+//                tau >= 1 keeps every key block that holds a real key.  In
+//                the fixed-ratio top-k mode (topk > 0; the ablation of Sec. 5,
+//                Table 2) the scan is skipped and s = min(topk, blocks holding
+//                a real key).  The kept blocks are flagged in a per-row byte
+//                mask and s is stored as the row's count.
 //   scan_counts  one workgroup: exclusive scan of the counts -> row_ptr.
 //   compact_rows one workgroup per row: the flagged block ids, ascending, at
 //                col_idx[row_ptr[r] ...].
@@ -29,7 +31,7 @@ __device__ __forceinline__ float clean_mass(float m) { return (m > 0.f) ? m : 0.
 template <int NKP>
 __global__ void __launch_bounds__(SEL_T)
     select_rows_kernel(const float* __restrict__ mass, int n_q, int n_k, int n_kv, int N,
-                       int block_q, float tau, int32_t* __restrict__ counts,
+                       int block_q, float tau, int topk, int32_t* __restrict__ counts,
                        uint8_t* __restrict__ flags) {
   constexpr int PER = NKP / SEL_T > 0 ? NKP / SEL_T : 1;  // sorted slots per thread
   __shared__ uint64_t key[NKP];
@@ -46,7 +48,7 @@ __global__ void __launch_bounds__(SEL_T)
     if (t == 0) counts[r] = 0;
     return;
   }
-  if (tau >= 1.0f) {
+  if (topk <= 0 && tau >= 1.0f) {
     for (int j = t; j < n_k; j += SEL_T) frow[j] = (j < n_kv) ? 1 : 0;
     if (t == 0) counts[r] = n_kv;
     return;
@@ -77,6 +79,16 @@ __global__ void __launch_bounds__(SEL_T)
       }
       __syncthreads();
     }
+  }
+
+  if (topk > 0) {  // fixed-ratio top-k: the first min(topk, n_kv) of the order
+    const int s = topk < n_kv ? topk : n_kv;
+    for (int p = t; p < n_k; p += SEL_T) {
+      const int j = (int)(uint32_t)key[p];
+      frow[j] = (p < s) ? 1 : 0;
+    }
+    if (t == 0) counts[r] = s;
+    return;
   }
 
   // fp64 inclusive scan: thread t owns sorted slots [t*PER, t*PER + PER)
@@ -178,9 +190,9 @@ __global__ void __launch_bounds__(SEL_T)
 
 template <int NKP>
 void launch_sel(const float* mass, int rows, int n_q, int n_k, int n_kv, int N, int block_q,
-                float tau, int32_t* counts, uint8_t* flags, hipStream_t stream) {
+                float tau, int topk, int32_t* counts, uint8_t* flags, hipStream_t stream) {
   hipLaunchKernelGGL(select_rows_kernel<NKP>, dim3(rows), dim3(SEL_T), 0, stream, mass, n_q, n_k,
-                     n_kv, N, block_q, tau, counts, flags);
+                     n_kv, N, block_q, tau, topk, counts, flags);
 }
 
 }  // namespace
@@ -193,7 +205,7 @@ size_t select_workspace_bytes(int rows, int n_k) {
 int select_max_nk() { return 4096; }
 
 hipError_t launch_select(const float* mass, int B, int H, int N, int block_q, int block_k,
-                         float tau, int32_t* row_ptr, int32_t* col_idx, void* workspace,
+                         float tau, int topk, int32_t* row_ptr, int32_t* col_idx, void* workspace,
                          hipStream_t stream) {
   const int n_pad = padded_len(N, block_q, block_k);
   const int n_q = n_pad / block_q, n_k = n_pad / block_k;
@@ -202,10 +214,10 @@ hipError_t launch_select(const float* mass, int B, int H, int N, int block_q, in
   int32_t* counts = static_cast<int32_t*>(workspace);
   uint8_t* flags =
       static_cast<uint8_t*>(workspace) + (((size_t)rows * 4 + 255) & ~(size_t)255);
-  if (n_k <= 64) launch_sel<64>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, counts, flags, stream);
-  else if (n_k <= 256) launch_sel<256>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, counts, flags, stream);
-  else if (n_k <= 1024) launch_sel<1024>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, counts, flags, stream);
-  else if (n_k <= 4096) launch_sel<4096>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, counts, flags, stream);
+  if (n_k <= 64) launch_sel<64>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, topk, counts, flags, stream);
+  else if (n_k <= 256) launch_sel<256>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, topk, counts, flags, stream);
+  else if (n_k <= 1024) launch_sel<1024>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, topk, counts, flags, stream);
+  else if (n_k <= 4096) launch_sel<4096>(mass, rows, n_q, n_k, n_kv, N, block_q, tau, topk, counts, flags, stream);
   else return hipErrorInvalidValue;
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

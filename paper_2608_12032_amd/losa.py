@@ -22,8 +22,9 @@ STATUS = {0: "LOSA_OK", 1: "LOSA_ERR_NULL_POINTER", 2: "LOSA_ERR_INVALID_SHAPE",
           3: "LOSA_ERR_INVALID_TAU", 4: "LOSA_ERR_ALIGNMENT", 5: "LOSA_ERR_UNSUPPORTED",
           6: "LOSA_ERR_CAPACITY", 7: "LOSA_ERR_HIP"}
 
-EXPORTED = ("losa_calibrate_mass", "losa_select_blocks", "losa_sparse_attn_fwd",
-            "losa_workspace_bytes", "losa_status_string", "losa_last_error", "losa_version")
+EXPORTED = ("losa_calibrate_mass", "losa_select_blocks", "losa_select_blocks_topk",
+            "losa_block_recall", "losa_sparse_attn_fwd", "losa_workspace_bytes",
+            "losa_status_string", "losa_last_error", "losa_version")
 
 
 class LosaError(RuntimeError):
@@ -41,6 +42,10 @@ def _load():
     lib.losa_calibrate_mass.restype = I
     lib.losa_select_blocks.argtypes = [P, I, I, I, I, I, F, P, P, L, P, Z, P]
     lib.losa_select_blocks.restype = I
+    lib.losa_select_blocks_topk.argtypes = [P, I, I, I, I, I, I, P, P, L, P, Z, P]
+    lib.losa_select_blocks_topk.restype = I
+    lib.losa_block_recall.argtypes = [P, I, I, I, I, I, P, P, L, P, P, P, Z, P]
+    lib.losa_block_recall.restype = I
     lib.losa_sparse_attn_fwd.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, L, P, P, P, Z, P]
     lib.losa_sparse_attn_fwd.restype = I
     lib.losa_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
@@ -139,6 +144,45 @@ def losa_select_blocks(mass, N: int, block_q: int, block_k: int | None, tau: flo
     return row_ptr, col_idx
 
 
+def losa_select_blocks_topk(mass, N: int, block_q: int, block_k: int | None, k: int,
+                            row_ptr=None, col_idx=None, workspace=None):
+    """Fixed-ratio top-k selection (k blocks per row) -> (row_ptr, col_idx buffer)."""
+    block_k = block_k or block_q
+    B, H, n_q, n_k = mass.shape
+    rows = B * H * n_q
+    dev = mass.device
+    if row_ptr is None:
+        row_ptr = torch.empty(rows + 1, dtype=torch.int32, device=dev)
+    if col_idx is None:
+        col_idx = torch.empty(rows * n_k, dtype=torch.int32, device=dev)
+    need = workspace_bytes(1, LOSA_DTYPE_F32, B, H, N, 1, block_q, block_k)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = lib.losa_select_blocks_topk(_ptr(mass), B, H, N, block_q, block_k, int(k),
+                                     _ptr(row_ptr), _ptr(col_idx), col_idx.numel(),
+                                     _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(st, "losa_select_blocks_topk")
+    return row_ptr, col_idx
+
+
+def losa_block_recall(mass, N: int, block_q: int, block_k: int | None, row_ptr, col_idx,
+                      want_rows: bool = True, want_heads: bool = True, workspace=None):
+    """Recall of a frozen support on these masses -> (recall_rows or None, recall_heads or None)."""
+    block_k = block_k or block_q
+    B, H, n_q, n_k = mass.shape
+    dev = mass.device
+    rec_rows = torch.empty(B * H * n_q, dtype=torch.float32, device=dev) if want_rows else None
+    rec_heads = torch.empty((B, H), dtype=torch.float32, device=dev) if want_heads else None
+    need = workspace_bytes(3, LOSA_DTYPE_F32, B, H, N, 1, block_q, block_k)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = lib.losa_block_recall(_ptr(mass), B, H, N, block_q, block_k, _ptr(row_ptr),
+                               _ptr(col_idx), col_idx.numel(), _ptr(rec_rows), _ptr(rec_heads),
+                               _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(st, "losa_block_recall")
+    return rec_rows, rec_heads
+
+
 def nnz(row_ptr) -> int:
     return int(row_ptr[-1].item())
 
@@ -172,4 +216,6 @@ def losa_sparse_attn_fwd(q, k, v, N: int, block_q: int, block_k: int | None, row
 # shorter aliases
 calibrate_mass = losa_calibrate_mass
 select_blocks = losa_select_blocks
+select_blocks_topk = losa_select_blocks_topk
+block_recall = losa_block_recall
 sparse_attn_fwd = losa_sparse_attn_fwd

@@ -104,6 +104,34 @@ def test_fwd_validation(L, kw, code):
     assert _fwd(L, **kw) == code
 
 
+def _topk(L, mass=FAKE, B=1, H=2, N=1000, bq=128, bk=32, k=5, rp=FAKE, ci=FAKE, cap=10**6,
+          ws=FAKE, wsb=10**7):
+    return L.lib.losa_select_blocks_topk(mass, B, H, N, bq, bk, k, rp, ci, cap, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=0), 2), (dict(k=-3), 2), (dict(mass=None), 1), (dict(ws=None), 1),
+    (dict(cap=16 * 32 - 1), 6), (dict(wsb=10), 6), (dict(ci=MIS), 4), (dict(bq=100), 2),
+])
+def test_select_topk_validation(L, kw, code):
+    # N=1000, blocks 128 x 32 -> N_pad 1024, rows 16, n_k 32
+    assert _topk(L, **kw) == code
+
+
+def _rec(L, mass=FAKE, B=1, H=2, N=1000, bq=128, bk=128, rp=FAKE, ci=FAKE, cl=100, rows=FAKE,
+         heads=FAKE, ws=FAKE, wsb=10**6):
+    return L.lib.losa_block_recall(mass, B, H, N, bq, bk, rp, ci, cl, rows, heads, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(mass=None), 1), (dict(rp=None), 1), (dict(ws=None), 1), (dict(ci=None), 1),
+    (dict(cl=-1), 2), (dict(H=0), 2), (dict(rows=MIS), 4), (dict(heads=MIS), 4),
+    (dict(wsb=16 * 16 - 1), 6), (dict(N=4097 * 128), 5),
+])
+def test_recall_validation(L, kw, code):
+    assert _rec(L, **kw) == code
+
+
 def test_workspace_sizes(L):
     B, H, N, d = 1, 12, 32760, 128
     assert L.workspace_bytes(0, 1, B, H, N, d, 128, 128) == 0
@@ -111,6 +139,7 @@ def test_workspace_sizes(L):
     assert L.workspace_bytes(2, 0, B, H, N, d, 128, 128) == 0
     rows, n_k = 12 * 256, 256
     assert L.workspace_bytes(1, 0, B, H, N, 1, 128, 128) == ((rows * 4 + 255) // 256) * 256 + rows * n_k
+    assert L.workspace_bytes(3, 0, B, H, N, 1, 128, 128) == rows * 16
     assert L.workspace_bytes(5, 1, B, H, N, d, 128, 128) == 0
     assert L.workspace_bytes(2, 1, 0, H, N, d, 128, 128) == 0
 

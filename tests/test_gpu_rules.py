@@ -1,0 +1,156 @@
+"""GPU parity of the selection-rule ablation and of recall tracking.
+
+* losa_select_blocks_topk, the fixed-ratio top-k rule (Sec. 5, Table 2),
+  against the oracle's select_blocks_topk on the same fp32 masses: the sets
+  must be identical (same order, same tie rule, no floating point involved).
+* losa_block_recall, Eq. (2) of a frozen support on the masses of a later
+  step (Sec. 3.1, 3.3), against the oracle's recall_rows / recall_heads on the
+  masses the GPU produced (tolerance 1e-6: fp64 sums returned as fp32) and on
+  the oracle's own masses of the same inputs (1e-4, the mass tolerance).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import losa_oracle as O
+from paper_2608_12032_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+REC_TOL = 1e-6
+MASS_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def L():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    from paper_2608_12032_amd import losa
+    return losa
+
+
+def say(msg):
+    print(f"[gpu-rules] {msg}", flush=True)
+
+
+def f64(x):
+    return x.detach().float().cpu().numpy().astype(np.float64)
+
+
+def host_csr(rp, ci):
+    rp_h = rp.cpu().numpy().astype(np.int64)
+    return rp_h, ci[:rp_h[-1]].cpu().numpy().astype(np.int64)
+
+
+CASES = {
+    "wan-small": W.scaled(W.WORKLOADS["wan"], grid=(4, 12, 30), H=3, name="wan-small"),
+    "wan-small-c32": W.rectangular(W.scaled(W.WORKLOADS["wan"], grid=(4, 12, 30), H=3,
+                                            name="wan-small")),
+    "tiny": W.WORKLOADS["tiny"],
+}
+
+
+@pytest.mark.parametrize("key", list(CASES))
+def test_topk_on_oracle_masses_is_exact(L, key):
+    w = CASES[key]
+    q, k, _ = W.make_inputs(w)
+    m_ref, _ = O.block_masses(q.float().numpy(), k.float().numpy(), w.N, w.block, w.bk, w.scale)
+    m32 = m_ref.astype(np.float32)
+    # force exact ties inside some rows: equal masses must go to the smaller id
+    m32.reshape(-1, w.n_kblocks)[::3, 1:4] = m32.reshape(-1, w.n_kblocks)[::3, 1:2]
+    mdev = torch.from_numpy(m32).cuda()
+    n_kv = O.num_valid_key_blocks(w.N, w.bk)
+    for kk in sorted({1, 2, max(1, n_kv // 3), n_kv - 1, n_kv, n_kv + 5}):
+        rp, ci = L.losa_select_blocks_topk(mdev, w.N, w.block, w.bk, kk)
+        torch.cuda.synchronize()
+        rp_g, ci_g = host_csr(rp, ci)
+        rp_o, ci_o, _ = O.select_blocks_topk(m32.astype(np.float64), w.N, w.block, w.bk, kk)
+        say(f"{key}: k={kk} nnz={rp_g[-1]}")
+        assert np.array_equal(rp_g, rp_o) and np.array_equal(ci_g, ci_o), kk
+
+
+@pytest.mark.parametrize("key", ["wan-small", "wan-small-c32"])
+def test_rules_at_matched_coverage(L, key):
+    # Table 2's comparison on synthetic inputs: the threshold rule and the
+    # top-k rule with the same average coverage; recall of both on the same
+    # masses, GPU against the oracle.  The threshold rule keeps >= tau per row.
+    w = CASES[key]
+    q, k, _ = W.make_inputs(w, device="cuda")
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk, want_lse=False)
+    rp_t, ci_t = L.losa_select_blocks(mass, w.N, w.block, w.bk, w.tau)
+    torch.cuda.synchronize()
+    rows = w.B * w.H * w.n_blocks
+    kk = max(1, round(L.nnz(rp_t) / rows))
+    rp_k, ci_k = L.losa_select_blocks_topk(mass, w.N, w.block, w.bk, kk)
+    torch.cuda.synchronize()
+    mg = f64(mass)
+    res = {}
+    for name, (rp, ci) in {"threshold": (rp_t, ci_t), "topk": (rp_k, ci_k)}.items():
+        rr, rh = L.losa_block_recall(mass, w.N, w.block, w.bk, rp, ci)
+        torch.cuda.synchronize()
+        rp_h, ci_h = host_csr(rp, ci)
+        want_r = O.recall_rows(mg, rp_h, ci_h)
+        want_h = O.recall_heads(mg, rp_h, ci_h, w.N, w.block)
+        assert np.abs(f64(rr) - want_r).max() <= REC_TOL
+        assert np.abs(f64(rh) - want_h).max() <= REC_TOL
+        res[name] = (rp_h[-1] / (rows * w.n_kblocks), float(want_h.mean()), float(want_h.min()))
+    say(f"{key}: k={kk} (coverage, mean head recall, worst head recall) {res}")
+    rp_h, ci_h = host_csr(rp_t, ci_t)
+    valid = np.array([(r % w.n_blocks) * w.block < w.N for r in range(rows)])
+    assert np.all(O.recall_rows(mg, rp_h, ci_h)[valid] >= np.float32(w.tau) - 1e-5)
+
+
+@pytest.mark.parametrize("key", ["wan-small", "wan-small-c32", "tiny"])
+def test_recall_of_frozen_support_across_drift(L, key):
+    # construct at step 0, then recall of that support on the masses of the
+    # drifted steps (the paper's frozen-pattern measurement), plus a support
+    # with repeated and stray ids
+    w = CASES[key]
+    state = W.make_state(w, device="cuda")
+    q, k, _ = W.cast(state, w)
+    mass0, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk, want_lse=False)
+    rp, ci = L.losa_select_blocks(mass0, w.N, w.block, w.bk, w.tau)
+    torch.cuda.synchronize()
+    rp_h, ci_h = host_csr(rp, ci)
+    rows = rp_h.size - 1
+    rng = np.random.default_rng(5)
+    dup = [np.concatenate([ci_h[rp_h[r]:rp_h[r + 1]],
+                           rng.choice(w.n_kblocks, 3), [-2, w.n_kblocks + 1]]) for r in range(rows)]
+    rp_d = np.concatenate([[0], np.cumsum([len(x) for x in dup])])
+    ci_d = np.concatenate(dup)
+    for step in range(1, 4):
+        W.drift_(state, w, step)
+        q, k, _ = W.cast(state, w)
+        mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk, want_lse=False)
+        m_ref, _ = O.block_masses(f64(q), f64(k), w.N, w.block, w.bk, w.scale)
+        mg = f64(mass)
+        for rp_x, ci_x in ((rp_h, ci_h), (rp_d, ci_d)):
+            rr, rh = L.losa_block_recall(mass, w.N, w.block, w.bk,
+                                         torch.from_numpy(rp_x.astype(np.int32)).cuda(),
+                                         torch.from_numpy(ci_x.astype(np.int32)).cuda())
+            torch.cuda.synchronize()
+            assert np.abs(f64(rr) - O.recall_rows(mg, rp_x, ci_x)).max() <= REC_TOL
+            assert np.abs(f64(rh) - O.recall_heads(mg, rp_x, ci_x, w.N, w.block)).max() <= REC_TOL
+            assert np.abs(f64(rh) - O.recall_heads(m_ref, rp_x, ci_x, w.N, w.block)).max() \
+                <= MASS_TOL
+        say(f"{key}: step {step} head recall {f64(rh).round(4).tolist()}")
+
+
+def test_recall_full_size_wan(L):
+    # every row of the Wan-shaped workload at the first reuse step
+    w = W.WORKLOADS["wan"]
+    state = W.make_state(w, device="cuda")
+    q, k, _ = W.cast(state, w)
+    mass0, _ = L.losa_calibrate_mass(q, k, w.N, w.block, want_lse=False)
+    rp, ci = L.losa_select_blocks(mass0, w.N, w.block, w.block, w.tau)
+    W.drift_(state, w, 1)
+    q, k, _ = W.cast(state, w)
+    del state
+    mass1, _ = L.losa_calibrate_mass(q, k, w.N, w.block, want_lse=False)
+    rr, rh = L.losa_block_recall(mass1, w.N, w.block, w.block, rp, ci)
+    torch.cuda.synchronize()
+    rp_h, ci_h = host_csr(rp, ci)
+    mg = f64(mass1)
+    assert np.abs(f64(rr) - O.recall_rows(mg, rp_h, ci_h)).max() <= REC_TOL
+    want_h = O.recall_heads(mg, rp_h, ci_h, w.N, w.block)
+    assert np.abs(f64(rh) - want_h).max() <= REC_TOL
+    say(f"wan full: step-1 recall mean {want_h.mean():.4f} worst head {want_h.min():.4f}")
