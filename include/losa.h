@@ -182,8 +182,35 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
                                  size_t workspace_bytes, void* stream);
 
 /*
+ * The construction step (Sec. 4.1; Sec. 5.1: one dense attention step that also
+ * yields the exact block masses).  Step t0 is a dense step, so the sampler
+ * needs its dense attention output anyway; this call returns it together with
+ * the masses that losa_select_blocks turns into the frozen support.
+ *
+ * o     out, [B][H][N_pad][d] of `dtype`: dense attention over all N valid
+ *       keys (Sec. 3.1), padding rows 0.
+ * mass  out, fp32 [B][H][n_q][n_k]: as losa_calibrate_mass.
+ * lse   out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp of the scaled
+ *       scores over all valid keys, -inf on padding.
+ * workspace  bf16: >= losa_workspace_bytes(4, ...) bytes (the sparse forward's
+ *       workspace, then room for lse when lse is NULL); f32: unused.
+ * bf16 runs the sparse forward's kernel over every valid key block (O and
+ * lse), then only the mass sweep of the calibration kernel with that lse: one
+ * dense attention plus one Q K^T sweep, instead of the calibration's two
+ * sweeps plus a separate dense attention.  The scores are bitwise those of the
+ * two other calls, so mass and lse agree with losa_calibrate_mass to fp32
+ * rounding and o with losa_sparse_attn_fwd over a full support exactly.
+ * f32 runs losa_calibrate_mass and a dense fp32 forward.
+ */
+losa_status losa_construct(const void* q, const void* k, const void* v, losa_dtype dtype, int B,
+                           int H, int N, int d, int block_q, int block_k, float scale, void* o,
+                           float* mass, float* lse, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
  * Workspace bytes needed by: which = 0 losa_calibrate_mass, 1 losa_select_blocks
- * and losa_select_blocks_topk, 2 losa_sparse_attn_fwd, 3 losa_block_recall.
+ * and losa_select_blocks_topk, 2 losa_sparse_attn_fwd, 3 losa_block_recall,
+ * 4 losa_construct (with lse NULL; with lse given, which = 2 suffices).
  * Returns 0 for invalid arguments (then the call itself reports the error).
  */
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,

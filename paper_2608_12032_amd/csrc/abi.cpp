@@ -109,7 +109,7 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
                   s.n_k);
     return hip_status(
         losa::launch_calibrate_bf16(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale, mass, lse,
-                                    hs),
+                                    false, hs),
         "losa_calibrate_mass");
   }
   return hip_status(
@@ -243,6 +243,55 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
                     "losa_sparse_attn_fwd");
 }
 
+losa_status losa_construct(const void* q, const void* k, const void* v, losa_dtype dtype, int B,
+                           int H, int N, int d, int block_q, int block_k, float scale, void* o,
+                           float* mass, float* lse, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  if (!q || !k || !v || !o || !mass)
+    return fail(LOSA_ERR_NULL_POINTER, "q, k, v, o and mass must be non-NULL");
+  Shape s;
+  losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
+  if (st != LOSA_OK) return st;
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite and > 0");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(mass) ||
+      (lse && !aligned16(lse)))
+    return fail(LOSA_ERR_ALIGNMENT, "tensor pointers must be 16-byte aligned");
+  st = check_supported(dtype, s);
+  if (st != LOSA_OK) return st;
+  if (s.n_k > losa::kSparseFwdMaxNk)
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per head exceeds %d", s.n_k,
+                losa::kSparseFwdMaxNk);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (dtype == LOSA_DTYPE_F32) {
+    // fp32: the calibration kernel's own two sweeps, then the dense forward
+    st = losa_calibrate_mass(q, k, dtype, B, H, N, d, block_q, block_k, scale, mass, lse,
+                             nullptr, 0, stream);
+    if (st != LOSA_OK) return st;
+    return hip_status(losa::launch_sparse_fwd_f32(d, block_q, block_k, q, k, v, B, H, N, s.n_pad,
+                                                  scale, nullptr, nullptr, 0, o, nullptr, hs),
+                      "losa_construct");
+  }
+  if (losa::calib_bf16_lds_bytes(d, block_q, s.n_k) > kMaxLds)
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks exceed the calibration LDS budget",
+                s.n_k);
+  const size_t fwd_ws = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q);
+  const size_t lse_off = (fwd_ws + 255) / 256 * 256;
+  const size_t need = lse ? fwd_ws : lse_off + (size_t)B * H * s.n_pad * sizeof(float);
+  if (!workspace) return fail(LOSA_ERR_NULL_POINTER, "bf16 needs a workspace of %zu bytes", need);
+  if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
+  if (workspace_bytes < need)
+    return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
+  float* l = lse ? lse : reinterpret_cast<float*>(static_cast<char*>(workspace) + lse_off);
+  st = hip_status(losa::launch_dense_bf16(d, block_q, block_k, q, k, v, B, H, N, s.n_pad, scale, o,
+                                          l, workspace, hs),
+                  "losa_construct (dense attention)");
+  if (st != LOSA_OK) return st;
+  return hip_status(losa::launch_calibrate_bf16(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale,
+                                                mass, l, true, hs),
+                    "losa_construct (block masses)");
+}
+
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
                             int block_k) {
   Shape s;
@@ -257,6 +306,11 @@ size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, in
       return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) : 0;
     case 3:
       return losa::recall_workspace_bytes((int)s.rows);
+    case 4:  // losa_construct, lse not passed (the larger of the two)
+      return dtype == LOSA_DTYPE_BF16
+                 ? (losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) + 255) / 256 * 256 +
+                       (size_t)B * H * s.n_pad * sizeof(float)
+                 : 0;
     default:
       return 0;
   }

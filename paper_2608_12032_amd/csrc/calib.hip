@@ -19,8 +19,10 @@
 //      per-tile partial in LDS and the workgroup adds the waves' partials in a
 //      fixed order at the end.  No atomics: the result is bitwise repeatable.
 // The MFMA orientation is the one of the sparse forward (one query per lane in
-// the S^T accumulator).  K tiles are double-buffered in LDS with direct
-// 16-byte loads; one barrier per tile.
+// the S^T accumulator), so the scores are bitwise those the forward computes.
+// K tiles are double-buffered in LDS with direct 16-byte loads; one barrier per
+// tile.  With LSE_IN the normaliser comes from the caller (the dense forward of
+// the construction step already produced it) and only sweep 2 runs.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -77,7 +79,7 @@ __device__ __forceinline__ void tile_scores(const char* buf, const bf16x8_t* qre
   }
 }
 
-template <int D, int BLK, int BK>
+template <int D, int BLK, int BK, bool LSE_IN>
 __global__ void __launch_bounds__(BLK * 2, 2)
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                       float* __restrict__ mass, float* __restrict__ lse, int rows_total, int n_q,
@@ -106,7 +108,7 @@ __global__ void __launch_bounds__(BLK * 2, 2)
 
   if (rows_valid <= 0) {  // a query block made only of padding
     for (int j = tid; j < n_k; j += C::NT) mrow[j] = 0.f;
-    if (lse != nullptr)
+    if (!LSE_IN && lse != nullptr)
       for (int t = tid; t < BLK; t += C::NT) lse[(size_t)bh * n_pad + i * BLK + t] = -INFINITY;
     return;
   }
@@ -121,6 +123,11 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   }
   const int n_kv = (N + BLK - 1) / BLK;  // key tiles holding a real key
 
+  const bool qvalid = qrow < N;
+  float lse2;
+  if constexpr (LSE_IN) {
+    lse2 = qvalid ? lse[(size_t)bh * n_pad + qrow] * kLog2e : 0.f;
+  } else {
   // ---- sweep 1: running max / sum -> lse (log2 units) ----------------------
   float m_run = kNegBig;
   float l_run = 0.f;
@@ -153,15 +160,15 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     m_run = mx;
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const bool qvalid = qrow < N;
-  const float lse2 = m_run + __log2f(l_tot);
+  lse2 = m_run + __log2f(l_tot);
   if (lse != nullptr && g == 0)
     lse[(size_t)bh * n_pad + qrow] = qvalid ? lse2 * kLn2 : -INFINITY;
+  }
   // padding rows contribute exp2(x - inf) = 0 to every mass
   const float sub = qvalid ? lse2 : INFINITY;
 
   // ---- sweep 2: block masses -----------------------------------------------
-  wait_vm_barrier<0>();  // all waves are done with the last tile of sweep 1
+  wait_vm_barrier<0>();  // all waves are done with the last tile of sweep 1 (or with nothing)
   issue_tile<D, BLK>(buf0, krs, 0, w, lane);
   for (int j = 0; j < n_kv; ++j) {
     char* cur = (j & 1) ? buf1 : buf0;
@@ -201,7 +208,7 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   }
 }
 
-template <int D, int BLK, int BK>
+template <int D, int BLK, int BK, bool LSE_IN>
 hipError_t launch_cal(const void* q, const void* k, int B, int H, int N, int n_pad, float scale,
                       float* mass, float* lse, hipStream_t stream) {
   using C = CalCfg<D, BLK>;
@@ -210,10 +217,10 @@ hipError_t launch_cal(const void* q, const void* k, int B, int H, int N, int n_p
   const int rows = B * H * n_q;
   const size_t lds = 2 * (size_t)C::TILE + (size_t)C::NW * n_k * sizeof(float);
   hipError_t err =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK, BK>),
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK, BK, LSE_IN>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(C::NT), lds, stream,
+  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK, BK, LSE_IN>), dim3(rows), dim3(C::NT), lds, stream,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), mass, lse,
                      rows, n_q, n_k, N, n_pad, scale * kLog2e);
   return hipGetLastError();
@@ -227,10 +234,11 @@ size_t calib_bf16_lds_bytes(int d, int blk, int n_k) {
 
 hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                  int H, int N, int n_pad, float scale, float* mass, float* lse,
-                                 hipStream_t stream) {
+                                 bool lse_in, hipStream_t stream) {
 #define LOSA_CAL(DD, BB, KK)                                                              \
   if (d == DD && blk == BB && blk_k == KK)                                                \
-    return launch_cal<DD, BB, KK>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+    return lse_in ? launch_cal<DD, BB, KK, true>(q, k, B, H, N, n_pad, scale, mass, lse, stream) \
+                  : launch_cal<DD, BB, KK, false>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
   LOSA_CAL(128, 128, 128)
   LOSA_CAL(64, 128, 128)
   LOSA_CAL(128, 64, 64)

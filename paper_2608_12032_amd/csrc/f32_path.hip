@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(BLK)
                           const float* __restrict__ V, const int32_t* __restrict__ row_ptr,
                           const int32_t* __restrict__ col_idx, int64_t col_len,
                           float* __restrict__ O, float* __restrict__ lse, int n_q, int n_k, int N,
-                          int n_pad, float scale_log2) {
+                          int n_pad, float scale_log2, int dense) {
   __shared__ __attribute__((aligned(16))) float Kc[CK * D];
   __shared__ __attribute__((aligned(16))) float Vc[CK * D];
   const int t = threadIdx.x;
@@ -54,15 +54,18 @@ __global__ void __launch_bounds__(BLK)
   }
   float m = kNegBig, l = 0.f;
 
+  // dense: every key block that holds a valid key (the construction step)
   __shared__ uint8_t flag[kSparseFwdMaxNk];
-  for (int j = t; j < n_k; j += BLK) flag[j] = 0;
+  for (int j = t; j < n_k; j += BLK) flag[j] = dense ? (j * BK < N) : 0;
   __syncthreads();
-  int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
-  e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
-  e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
-  for (int64_t e = e0 + t; e < e1; e += BLK) {
-    const int j = col_idx[e];
-    if (j >= 0 && j < n_k) flag[j] = 1;
+  if (!dense) {
+    int64_t e0 = row_ptr[r], e1 = row_ptr[r + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_len ? col_len : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_len ? col_len : e1);
+    for (int64_t e = e0 + t; e < e1; e += BLK) {
+      const int j = col_idx[e];
+      if (j >= 0 && j < n_k) flag[j] = 1;
+    }
   }
   __syncthreads();
   for (int j = 0; j < n_k; ++j) {
@@ -196,12 +199,12 @@ __global__ void __launch_bounds__(BLK)
 template <int D, int BLK, int BK>
 hipError_t launch_f32(const void* q, const void* k, const void* v, int B, int H, int N, int n_pad,
                       float scale, const int32_t* row_ptr, const int32_t* col_idx,
-                      int64_t col_len, void* o, float* lse, hipStream_t stream) {
+                      int64_t col_len, void* o, float* lse, int dense, hipStream_t stream) {
   const int n_q = n_pad / BLK, n_k = n_pad / BK;
   hipLaunchKernelGGL((sparse_fwd_f32_kernel<D, BLK, BK>), dim3(B * H * n_q), dim3(BLK), 0, stream,
                      static_cast<const float*>(q), static_cast<const float*>(k),
                      static_cast<const float*>(v), row_ptr, col_idx, col_len,
-                     static_cast<float*>(o), lse, n_q, n_k, N, n_pad, scale * kLog2e);
+                     static_cast<float*>(o), lse, n_q, n_k, N, n_pad, scale * kLog2e, dense);
   return hipGetLastError();
 }
 
@@ -221,10 +224,11 @@ hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const
                                  const void* v, int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,
                                  void* o, float* lse, hipStream_t stream) {
+  const int dense = row_ptr == nullptr;  // internal: the construction step's dense attention
 #define LOSA_F32_FWD(DD, BB, KK)                                                               \
   if (d == DD && blk == BB && blk_k == KK)                                                     \
     return launch_f32<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, row_ptr, col_idx, col_len, o, \
-                                  lse, stream);
+                                  lse, dense, stream);
   LOSA_F32_FWD(64, 64, 64)
   LOSA_F32_FWD(64, 128, 128)
   LOSA_F32_FWD(128, 64, 64)

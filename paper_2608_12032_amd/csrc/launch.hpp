@@ -16,9 +16,11 @@ __host__ __device__ inline int padded_len(int N, int block_q, int block_k) {
 }
 
 // blk = query block rows, blk_k = key block keys (blk, or 32)
+// lse_in: lse holds the natural-log normalisers already (from the dense
+// forward of the construction step) and only the mass sweep runs
 hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                  int H, int N, int n_pad, float scale, float* mass, float* lse,
-                                 hipStream_t stream);
+                                 bool lse_in, hipStream_t stream);
 hipError_t launch_calibrate_f32(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                 int H, int N, int n_pad, float scale, float* mass, float* lse,
                                 hipStream_t stream);
@@ -36,6 +38,10 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, cons
                                   const int32_t* row_ptr, const int32_t* col_idx,
                                   int64_t col_len, void* o, float* lse, void* workspace,
                                   hipStream_t stream);
+// dense attention over every valid key (row_ptr == nullptr for the f32 path)
+hipError_t launch_dense_bf16(int d, int blk, int blk_k, const void* q, const void* k,
+                             const void* v, int B, int H, int N, int n_pad, float scale, void* o,
+                             float* lse, void* workspace, hipStream_t stream);
 hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const void* k,
                                  const void* v, int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,

@@ -318,7 +318,7 @@ __global__ void __launch_bounds__(BLK * 2)
                            const int32_t* __restrict__ col_idx, int64_t col_len,
                            __bf16* __restrict__ O, float* __restrict__ lse,
                            const int* __restrict__ order, int n_q, int n_k, int N, int n_pad,
-                           float scale_log2) {
+                           float scale_log2, int dense) {
   using C = FwdCfg<D, BLK, BK>;
   constexpr int NS = C::NS;
   constexpr int R = C::R;
@@ -333,7 +333,10 @@ __global__ void __launch_bounds__(BLK * 2)
   const int l32 = lane & 31;
   const int g = lane >> 5;
 
-  const int r = order[blockIdx.x];
+  // dense: every row keeps every key block that holds a valid key (the dense
+  // attention of the construction step); rows run in id order, each XCD on a
+  // contiguous range of them
+  const int r = dense ? xcd_remap(blockIdx.x, gridDim.x) : order[blockIdx.x];
   const int bh = r / n_q;
   const int qb = r - bh * n_q;
   const size_t head = (size_t)bh * n_pad * D;
@@ -344,7 +347,11 @@ __global__ void __launch_bounds__(BLK * 2)
   // ---- the row's distinct valid key blocks, ascending ---------------------
   // (flags and per-wave counts live in the rings, unused until the first load)
   int nb = 0;
-  {
+  if (dense) {
+    nb = (N + BK - 1) / BK;
+    for (int j = tid; j < nb; j += C::NT) list[j] = (uint16_t)j;
+    __syncthreads();
+  } else {
     uint8_t* const flag = reinterpret_cast<uint8_t*>(smem);
     int* const wcount = reinterpret_cast<int*>(smem + kMaxList);
     for (int j = tid; j < n_k; j += C::NT) flag[j] = 0;
@@ -691,7 +698,28 @@ hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H,
   hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(FwdCfg<D, BLK, BK>::NT), 0,
                      stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(vt), row_ptr, col_idx, col_len,
-                     static_cast<__bf16*>(o), lse, order, n_q, n_k, N, n_pad, scale * kLog2e);
+                     static_cast<__bf16*>(o), lse, order, n_q, n_k, N, n_pad, scale * kLog2e, 0);
+  return hipGetLastError();
+}
+
+// Dense attention of every query block over every valid key (the forward
+// kernel with full rows): O and lse of the construction step.
+template <int D, int BLK, int BK>
+hipError_t launch_dense(const void* q, const void* k, const void* v, int B, int H, int N,
+                        int n_pad, float scale, void* o, float* lse, void* workspace,
+                        hipStream_t stream) {
+  const int BH = B * H;
+  const int n_q = n_pad / BLK;
+  const int n_k = n_pad / BK;
+  const int rows = BH * n_q;
+  __bf16* vt = static_cast<__bf16*>(workspace);
+  dim3 tgrid(n_pad / 64, BH);
+  hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
+                     static_cast<const __bf16*>(v), vt, n_pad);
+  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(FwdCfg<D, BLK, BK>::NT),
+                     0, stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
+                     static_cast<const __bf16*>(vt), nullptr, nullptr, 0, static_cast<__bf16*>(o),
+                     lse, nullptr, n_q, n_k, N, n_pad, scale * kLog2e, 1);
   return hipGetLastError();
 }
 
@@ -715,6 +743,24 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, cons
   LOSA_FWD(128, 64, 32)
   LOSA_FWD(64, 64, 32)
 #undef LOSA_FWD
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_dense_bf16(int d, int blk, int blk_k, const void* q, const void* k,
+                             const void* v, int B, int H, int N, int n_pad, float scale, void* o,
+                             float* lse, void* workspace, hipStream_t stream) {
+#define LOSA_DENSE(DD, BB, KK)                                                                 \
+  if (d == DD && blk == BB && blk_k == KK)                                                     \
+    return launch_dense<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, o, lse, workspace, stream);
+  LOSA_DENSE(128, 128, 128)
+  LOSA_DENSE(64, 128, 128)
+  LOSA_DENSE(128, 64, 64)
+  LOSA_DENSE(64, 64, 64)
+  LOSA_DENSE(128, 128, 32)
+  LOSA_DENSE(64, 128, 32)
+  LOSA_DENSE(128, 64, 32)
+  LOSA_DENSE(64, 64, 32)
+#undef LOSA_DENSE
   return hipErrorInvalidValue;
 }
 

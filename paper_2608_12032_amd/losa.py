@@ -23,7 +23,7 @@ STATUS = {0: "LOSA_OK", 1: "LOSA_ERR_NULL_POINTER", 2: "LOSA_ERR_INVALID_SHAPE",
           6: "LOSA_ERR_CAPACITY", 7: "LOSA_ERR_HIP"}
 
 EXPORTED = ("losa_calibrate_mass", "losa_select_blocks", "losa_select_blocks_topk",
-            "losa_block_recall", "losa_sparse_attn_fwd", "losa_workspace_bytes",
+            "losa_block_recall", "losa_sparse_attn_fwd", "losa_construct", "losa_workspace_bytes",
             "losa_status_string", "losa_last_error", "losa_version")
 
 
@@ -48,6 +48,8 @@ def _load():
     lib.losa_block_recall.restype = I
     lib.losa_sparse_attn_fwd.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, L, P, P, P, Z, P]
     lib.losa_sparse_attn_fwd.restype = I
+    lib.losa_construct.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, P, P, Z, P]
+    lib.losa_construct.restype = I
     lib.losa_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
     lib.losa_workspace_bytes.restype = Z
     lib.losa_status_string.argtypes = [I]
@@ -213,9 +215,41 @@ def losa_sparse_attn_fwd(q, k, v, N: int, block_q: int, block_k: int | None, row
     return (o, lse) if want_lse else o
 
 
+def losa_construct(q, k, v, N: int, block_q: int, block_k: int | None = None,
+                   scale: float | None = None, want_lse: bool = False, out=None, mass=None,
+                   lse=None, workspace=None):
+    """Construction step: dense attention output and exact block masses of the
+    same step -> (o, mass) or (o, mass, lse)."""
+    block_k = block_k or block_q
+    B, H, Np, d = _qkv_shape(q)
+    for t in (k, v):
+        if t.shape != q.shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError("q, k, v must share shape/dtype and be contiguous")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    dcode = _dtype_code(q)
+    o = torch.empty_like(q) if out is None else out
+    if mass is None:
+        mass = torch.empty((B, H, Np // block_q, Np // block_k), dtype=torch.float32,
+                           device=q.device)
+    if want_lse and lse is None:
+        lse = torch.empty((B, H, Np), dtype=torch.float32, device=q.device)
+    if not want_lse:
+        lse = None
+    need = workspace_bytes(4 if lse is None else 2, dcode, B, H, N, d, block_q, block_k)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.losa_construct(_ptr(q), _ptr(k), _ptr(v), dcode, B, H, N, d, block_q, block_k, scale,
+                            _ptr(o), _ptr(mass), _ptr(lse), _ptr(workspace), ws_bytes,
+                            _stream(q.device))
+    _check(st, "losa_construct")
+    return (o, mass, lse) if want_lse else (o, mass)
+
+
 # shorter aliases
 calibrate_mass = losa_calibrate_mass
 select_blocks = losa_select_blocks
 select_blocks_topk = losa_select_blocks_topk
 block_recall = losa_block_recall
 sparse_attn_fwd = losa_sparse_attn_fwd
+construct = losa_construct

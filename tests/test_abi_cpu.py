@@ -132,6 +132,21 @@ def test_recall_validation(L, kw, code):
     assert _rec(L, **kw) == code
 
 
+def _con(L, q=FAKE, dtype=1, B=1, H=2, N=1000, d=128, bq=128, bk=128, o=FAKE, mass=FAKE,
+         lse=None, ws=FAKE, wsb=10**9, scale=0.1):
+    return L.lib.losa_construct(q, q, q, dtype, B, H, N, d, bq, bk, scale, o, mass, lse, ws, wsb,
+                                None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), 1), (dict(o=None), 1), (dict(mass=None), 1), (dict(ws=None), 1),
+    (dict(B=0), 2), (dict(scale=0.0), 2), (dict(o=MIS), 4), (dict(lse=MIS), 4),
+    (dict(d=96), 5), (dict(bq=128, bk=64), 5), (dict(wsb=100), 6),
+])
+def test_construct_validation(L, kw, code):
+    assert _con(L, **kw) == code
+
+
 def test_workspace_sizes(L):
     B, H, N, d = 1, 12, 32760, 128
     assert L.workspace_bytes(0, 1, B, H, N, d, 128, 128) == 0
@@ -140,6 +155,8 @@ def test_workspace_sizes(L):
     rows, n_k = 12 * 256, 256
     assert L.workspace_bytes(1, 0, B, H, N, 1, 128, 128) == ((rows * 4 + 255) // 256) * 256 + rows * n_k
     assert L.workspace_bytes(3, 0, B, H, N, 1, 128, 128) == rows * 16
+    fwd = L.workspace_bytes(2, 1, B, H, N, d, 128, 128)
+    assert L.workspace_bytes(4, 1, B, H, N, d, 128, 128) == (fwd + 255) // 256 * 256 + H * 32768 * 4
     assert L.workspace_bytes(5, 1, B, H, N, d, 128, 128) == 0
     assert L.workspace_bytes(2, 1, 0, H, N, d, 128, 128) == 0
 

@@ -154,3 +154,66 @@ def test_recall_full_size_wan(L):
     want_h = O.recall_heads(mg, rp_h, ci_h, w.N, w.block)
     assert np.abs(f64(rh) - want_h).max() <= REC_TOL
     say(f"wan full: step-1 recall mean {want_h.mean():.4f} worst head {want_h.min():.4f}")
+
+
+# ----------------------------------------------------------------------------
+# the construction step: dense attention output + exact block masses
+# ----------------------------------------------------------------------------
+
+CONSTRUCT = dict(CASES, **{
+    "cog-small": W.scaled(W.WORKLOADS["cog"], grid=(3, 10, 45), H=4, name="cog-small"),
+    "tiny-c32": W.rectangular(W.WORKLOADS["tiny"]),
+})
+OUT_TOL = {"bf16": (2e-2, 2e-3), "f32": (1e-4, 1e-4)}
+
+
+@pytest.mark.parametrize("key", list(CONSTRUCT))
+def test_construct_matches_oracle_and_the_separate_calls(L, key):
+    w = CONSTRUCT[key]
+    q, k, v = W.make_inputs(w, device="cuda")
+    o, mass, lse = L.losa_construct(q, k, v, w.N, w.block, w.bk, want_lse=True)
+    o2, mass2 = L.losa_construct(q, k, v, w.N, w.block, w.bk)   # lse kept in the workspace
+    m_cal, l_cal = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk)
+    rp, ci = L.losa_select_blocks(m_cal, w.N, w.block, w.bk, 1.0)
+    o_full = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.bk, rp, ci)
+    torch.cuda.synchronize()
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    o_ref, l_ref = O.dense_attention(qh, kh, vh, w.N, w.scale)
+    m_ref, _ = O.block_masses(qh, kh, w.N, w.block, w.bk, w.scale)
+    tmax, tmean = OUT_TOL[w.dtype]
+    err = np.abs(f64(o)[:, :, :w.N] - o_ref[:, :, :w.N])
+    say(f"construct {key}: out max {err.max():.2e} mean {err.mean():.2e}")
+    assert err.max() <= tmax and err.mean() <= tmean
+    assert np.all(f64(o)[:, :, w.N:] == 0)
+    assert np.abs(f64(mass) - m_ref).max() <= MASS_TOL
+    lg = f64(lse)
+    assert np.abs(lg[:, :, :w.N] - l_ref[:, :, :w.N]).max() <= 1e-3
+    assert np.all(np.isneginf(lg[:, :, w.N:]))
+    # the same scores as the separate calls: O exactly the forward over the
+    # full support, masses and lse to fp32 rounding of the normaliser
+    assert torch.equal(o, o_full) and torch.equal(o, o2) and torch.equal(mass, mass2)
+    assert np.abs(f64(mass) - f64(m_cal)).max() <= 1e-6
+    assert np.abs(lg[:, :, :w.N] - f64(l_cal)[:, :, :w.N]).max() <= 1e-5
+
+
+def test_construct_full_size_wan_sampled(L):
+    w = W.WORKLOADS["wan"]
+    q, k, v = W.make_inputs(w, device="cuda")
+    o, mass = L.losa_construct(q, k, v, w.N, w.block)
+    torch.cuda.synchronize()
+    n_q = w.n_blocks
+    heads, blocks = (0, w.H - 1), (0, n_q // 2, n_q - 1)
+    rows = [h * n_q + i for h in heads for i in blocks]
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    m_ref, _ = O.block_masses(qh, kh, w.N, w.block, w.block, w.scale, rows_subset=rows)
+    rp_full = np.arange(0, (w.H * n_q + 1) * n_q, n_q)
+    ci_full = np.tile(np.arange(n_q), w.H * n_q)
+    o_ref, _ = O.sparse_attention(qh, kh, vh, w.N, w.block, w.block, w.scale, rp_full, ci_full,
+                                  rows_subset=rows)
+    mg, og = f64(mass), f64(o)
+    for r in rows:
+        h, i = divmod(r, n_q)
+        assert np.abs(mg[0, h, i] - m_ref[0, h, i]).max() <= MASS_TOL
+        lo, hi = i * w.block, min((i + 1) * w.block, w.N)
+        err = np.abs(og[0, h, lo:hi] - o_ref[0, h, lo:hi])
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3
