@@ -3,10 +3,15 @@
 
 One step = one layer's whole LoSA cycle on the Wan2.1-1.3B-shaped workload
 (B=1, H=12, d=128, N=32,760 padded to 32,768, block 128, tau=0.99, bf16):
-  losa_calibrate_mass (exact block masses of the dense construction step)
+  losa_construct (the dense construction step: its attention output and the
+     exact block masses)
   -> losa_select_blocks (shortest prefix reaching tau, CSR)
   -> 49 x losa_sparse_attn_fwd over the frozen support, each on that reuse
      step's drifted Q/K/V.
+After the timed steps (untimed for the step clock): standalone calibration
+and dense-attention times for comparison, and the recall of the frozen
+support at later steps (Eq. (2)) next to the fixed-ratio top-k rule at the
+same coverage.
 All inputs (the calibration step and every drifted reuse step) are generated
 on the device before the timed region.  HIP events on the stream the library
 launches on time each call; the wall clock brackets the K timed steps.
@@ -50,6 +55,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense-compare", action="store_true",
+                    help="skip the untimed dense-attention comparison, which runs the sparse "
+                         "kernel over a full support (for profiles of the sparse launches alone)")
     ap.add_argument("--copy-reference-mib", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB, a "
                          "reference of known size for hardware byte counters")
@@ -82,9 +90,16 @@ def measured_traffic(workload: str):
     return rec
 
 
-KERNELS = {"sparse_fwd": "sparse_fwd_bf16_kernel", "transpose_v": "transpose_v_kernel",
-           "calibrate": "calib_bf16_kernel", "select_rows": "select_rows_kernel",
-           "compact_rows": "compact_rows_kernel"}
+# kernel-name substrings that identify each launch in a counter file.  The
+# forward kernel's name comes mangled (its last template flag: Lb0E sparse,
+# Lb1E dense); the calibration kernel's demangled (false: two sweeps, true:
+# one sweep with block statistics).
+KERNELS = {"sparse_fwd": ("sparse_fwd_bf16_kernel", "Lb0E"),
+           "dense_fwd": ("sparse_fwd_bf16_kernel", "Lb1E"),
+           "transpose_v": ("transpose_v_kernel",), "calibrate": ("calib_bf16_kernel", "true>"),
+           "stat_mass": ("stat_mass_kernel",),
+           "calibrate_two_sweep": ("calib_bf16_kernel", "false>"),
+           "select_rows": ("select_rows_kernel",), "compact_rows": ("compact_rows_kernel",)}
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
@@ -117,8 +132,8 @@ def record_traffic(fetch_csv: str, write_csv: str, copy_mib: int, workload: str)
             sys.exit(f"{path}: no {COPY_KERNEL} dispatch (run with --copy-reference-mib)")
         scale = copy_mib * 1024.0 / max(copies)   # known KiB / counted KiB
         res[counter.lower() + "_scale"] = round(scale, 4)
-        for key, pat in KERNELS.items():
-            vals = [v for n, v in per.values() if pat in n]
+        for key, pats in KERNELS.items():
+            vals = [v for n, v in per.values() if all(p in n for p in pats)]
             if vals:
                 k = res["kernels"].setdefault(key, {"launches": len(vals)})
                 k[counter.lower().replace("_size", "_bytes")] = int(sum(vals) / len(vals) * scale * 1024)
@@ -149,16 +164,16 @@ def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
     ci_h = ci[:rp_h[-1]].cpu().numpy().astype(np.int64)
     rows = rp_h.size - 1
     order = np.random.default_rng(0).permutation(rows)
-    t0 = time.perf_counter()
-    O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
-                       rows_subset=order[:4])
-    per_row = (time.perf_counter() - t0) / 4
-    n = int(min(rows, max(8, budget_s / max(per_row, 1e-6))))
-    sample = order[:n]
-    t0 = time.perf_counter()
-    O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
-                       rows_subset=sample)
-    dt = time.perf_counter() - t0
+    # rows in chunks, in a fixed random order, until the time budget is spent
+    n, dt, chunk = 0, 0.0, 8
+    while n < rows and dt < budget_s:
+        part = order[n:n + chunk]
+        t0 = time.perf_counter()
+        O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
+                           rows_subset=part)
+        dt += time.perf_counter() - t0
+        n += part.size
+        chunk = min(2 * chunk, 64)
     ms_layer = dt / n * rows * 1e3
     return {"value": round(ms_layer, 1), "unit": "ms/layer", "cores": int(threads),
             "kind": "oracle",
@@ -205,6 +220,9 @@ def main():
     del state
     dev = q0.device
     mass = torch.empty((w.B, w.H, n_q, n_k), dtype=torch.float32, device=dev)
+    out0 = torch.empty_like(q0)
+    ws_con = torch.empty(max(L.workspace_bytes(4, 1 if w.dtype == "bf16" else 0, w.B, w.H, N, d,
+                                               C, Ck), 16), dtype=torch.uint8, device=dev)
     row_ptr = torch.empty(rows + 1, dtype=torch.int32, device=dev)
     col_idx = torch.empty(rows * n_k, dtype=torch.int32, device=dev)
     ws_sel = torch.empty(max(L.workspace_bytes(1, 0, w.B, w.H, N, 1, C, Ck), 16),
@@ -225,7 +243,7 @@ def main():
     def step():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 + 2 * reuse)]
         ev[0].record()
-        L.losa_calibrate_mass(q0, k0, N, C, Ck, want_lse=False, mass=mass)
+        L.losa_construct(q0, k0, v0, N, C, Ck, out=out0, mass=mass, workspace=ws_con)
         ev[1].record()
         L.losa_select_blocks(mass, N, C, Ck, tau, row_ptr=row_ptr, col_idx=col_idx,
                              workspace=ws_sel)
@@ -244,7 +262,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    cal_ms = [e[0].elapsed_time(e[1]) for e in events]
+    con_ms = [e[0].elapsed_time(e[1]) for e in events]
     sel_ms = [e[1].elapsed_time(e[2]) for e in events]
     fwd_ms = [e[3 + 2 * t].elapsed_time(e[4 + 2 * t]) for e in events for t in range(reuse)]
     nnz = L.nnz(row_ptr)
@@ -263,8 +281,58 @@ def main():
     alg = {"sparse_fwd": 4 * qkv + 4 * (rows + 1 + nnz),
            "calibrate": 2 * qkv + mass_b,
            "select": mass_b + 4 * (rows + 1 + nnz)}
-    cal_t = sum(cal_ms) / len(cal_ms)
+    con_t = sum(con_ms) / len(con_ms)
     sel_t = sum(sel_ms) / len(sel_ms)
+
+    # ---- untimed comparisons: calibration alone, dense attention alone ------
+    def timed(fn, reps=5):
+        fn()
+        evs = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in evs) / reps
+
+    mass_cal = torch.empty_like(mass)
+    ws_cal = torch.empty(max(L.workspace_bytes(0, 1 if w.dtype == "bf16" else 0, w.B, w.H, N, d,
+                                               C, Ck), 16), dtype=torch.uint8, device=dev)
+    cal_t = timed(lambda: L.losa_calibrate_mass(q0, k0, N, C, Ck, want_lse=False, mass=mass_cal,
+                                                workspace=ws_cal))
+    cal2_t = timed(lambda: L.losa_calibrate_mass(q0, k0, N, C, Ck, want_lse=False, mass=mass_cal,
+                                                 two_sweep=True))
+    dense_t = None
+    if not args.no_dense_compare:
+        rp_full, ci_full = L.losa_select_blocks(mass_cal, N, C, Ck, 1.0)
+        dense_t = timed(lambda: L.losa_sparse_attn_fwd(q0, k0, v0, N, C, Ck, rp_full, ci_full,
+                                                       out=out, workspace=ws_fwd))
+        del rp_full, ci_full
+
+    # ---- recall of the frozen support at later steps (Eq. (2)) --------------
+    recall = {}
+    for t in sorted({1, (reuse + 1) // 2, reuse}):
+        if t < 1 or t > reuse:
+            continue
+        q, k, _ = reuse_inputs[t - 1]
+        L.losa_calibrate_mass(q, k, N, C, Ck, want_lse=False, mass=mass_cal, workspace=ws_cal)
+        _, rh = L.losa_block_recall(mass_cal, N, C, Ck, row_ptr, col_idx, want_rows=False)
+        rh = rh.float().cpu()
+        recall[f"step{t}"] = {"mean": round(float(rh.mean()), 5), "worst_head": round(float(rh.min()), 5)}
+    kk = max(1, round(nnz / rows))
+    rp_k, ci_k = L.losa_select_blocks_topk(mass, N, C, Ck, kk)
+    _, rh_k = L.losa_block_recall(mass, N, C, Ck, rp_k, ci_k, want_rows=False)
+    _, rh_t = L.losa_block_recall(mass, N, C, Ck, row_ptr, col_idx, want_rows=False)
+    recall["construction_step"] = {
+        "threshold_rule": {"coverage": round(nnz / (rows * n_k), 4),
+                           "mean": round(float(rh_t.float().mean()), 5),
+                           "worst_head": round(float(rh_t.float().min()), 5)},
+        "topk_rule_same_coverage": {"k": kk, "coverage": round(L.nnz(rp_k) / (rows * n_k), 4),
+                                    "mean": round(float(rh_k.float().mean()), 5),
+                                    "worst_head": round(float(rh_k.float().min()), 5)}}
+    del rp_k, ci_k, ws_cal
     hbm = {"calibrate": {"algorithmic_GBs": round(alg["calibrate"] / cal_t / 1e6, 1)},
            "select": {"algorithmic_GBs": round(alg["select"] / sel_t / 1e6, 1)},
            "note": "algorithmic bytes / measured time; counted_GBs = rocprofv3 FETCH_SIZE + "
@@ -272,7 +340,8 @@ def main():
     if traffic:
         kb = traffic["kernels"]
         tot = lambda key: kb.get(key, {}).get("fetch_bytes", 0) + kb.get(key, {}).get("write_bytes", 0)  # noqa: E731
-        hbm["calibrate"]["counted_GBs"] = round(tot("calibrate") / cal_t / 1e6, 1)
+        hbm["calibrate"]["counted_GBs"] = round((tot("calibrate") + tot("stat_mass")) / cal_t / 1e6,
+                                                1)
         hbm["select"]["counted_GBs"] = round((tot("select_rows") + tot("compact_rows")) / sel_t / 1e6, 1)
 
     res = {
@@ -292,15 +361,20 @@ def main():
             "workload": f"{w.name}-shaped: B={w.B} H={w.H} d={d} N={N} (padded {w.N_pad}) "
                         f"grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]} "
                         + (f"block {C}" if Ck == C else f"blocks {C}x{Ck}") + f" tau={tau}",
-            "step": f"calibrate + select + {reuse} reuse sparse forwards",
+            "step": f"construct (dense output + block masses) + select + {reuse} reuse sparse "
+                    "forwards",
             "reuse_steps": reuse,
             "nnz_blocks": nnz,
             "retained_fraction": round(nnz / (rows * n_k), 4),
         },
         "fwd_ms": {"mean": round(fwd, 4), "median": round(fwd_sorted[len(fwd_sorted) // 2], 4),
                    "min": round(fwd_sorted[0], 4)},
-        "calibrate_ms": round(sum(cal_ms) / len(cal_ms), 3),
-        "select_ms": round(sum(sel_ms) / len(sel_ms), 3),
+        "construct_ms": round(con_t, 3),
+        "select_ms": round(sel_t, 3),
+        "calibrate_alone_ms": round(cal_t, 3),
+        "calibrate_two_sweep_ms": round(cal2_t, 3),
+        "dense_attn_ms": round(dense_t, 3) if dense_t else None,
+        "construct_over_dense": round(con_t / dense_t, 3) if dense_t else None,
         "retained_tflops": round(achieved, 1),
         "dense_equiv_tflops": round(dense_flop / (fwd * 1e-3) / 1e12, 1),
         "kernel_speedup_vs_dense_flops": round(dense_flop / retained_flop, 3),
@@ -314,6 +388,7 @@ def main():
             "traffic_algorithmic": alg["sparse_fwd"],
         },
         "hbm": hbm,
+        "recall": recall,
     }
     if not args.no_cpu_baseline:
         q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)

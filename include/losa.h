@@ -70,9 +70,20 @@ typedef enum { LOSA_DTYPE_F32 = 0, LOSA_DTYPE_BF16 = 1 } losa_dtype;
  * mass       out, fp32 [B][H][n_q][n_k].
  * lse        out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp of the
  *            scaled scores of each query over all valid keys; -inf on padding.
- * workspace  unused in v1 (may be NULL; losa_workspace_bytes(0, ...) = 0).
+ * workspace  bf16, optional.  NULL: two sweeps over the keys per query block,
+ *            the first for lse, the second for the masses; no extra memory.
+ *            Non-NULL: one sweep that also stores, for every query q and key
+ *            block j, log2 of q's unnormalised probability sum over block j
+ *            (4 bytes each); a reduction with lse then gives the masses.  It
+ *            must hold at least one head's share, which is
+ *            losa_workspace_bytes(0, dtype, 1, 1, N, d, block_q, block_k);
+ *            heads are processed as many at a time as it holds, and
+ *            losa_workspace_bytes(0, ...) suggests room for all of them, up to
+ *            4 GiB.  Contents on entry are ignored and overwritten.  f32:
+ *            ignored (two sweeps).
  * Arithmetic: bf16 inputs use bf16 matrix-core products with fp32
- * accumulation; f32 inputs use fp32 throughout.
+ * accumulation; f32 inputs use fp32 throughout.  Both bf16 schemes compute
+ * the same scores; their masses differ only by fp32 rounding.
  */
 losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, int B, int H,
                                 int N, int d, int block_q, int block_k, float scale, float* mass,
@@ -192,14 +203,19 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
  * mass  out, fp32 [B][H][n_q][n_k]: as losa_calibrate_mass.
  * lse   out, nullable, fp32 [B][H][N_pad]: natural-log logsumexp of the scaled
  *       scores over all valid keys, -inf on padding.
- * workspace  bf16: >= losa_workspace_bytes(4, ...) bytes (the sparse forward's
- *       workspace, then room for lse when lse is NULL); f32: unused.
- * bf16 runs the sparse forward's kernel over every valid key block (O and
- * lse), then only the mass sweep of the calibration kernel with that lse: one
- * dense attention plus one Q K^T sweep, instead of the calibration's two
- * sweeps plus a separate dense attention.  The scores are bitwise those of the
- * two other calls, so mass and lse agree with losa_calibrate_mass to fp32
- * rounding and o with losa_sparse_attn_fwd over a full support exactly.
+ * workspace  bf16: required, at least one head's share, which is
+ *       losa_workspace_bytes(4, dtype, 1, 1, N, d, block_q, block_k); heads
+ *       are processed as many at a time as it holds, and
+ *       losa_workspace_bytes(4, ...) suggests room for all of them, up to
+ *       4 GiB.  f32: unused.
+ * bf16 runs the sparse forward's kernel over every valid key block.  Besides
+ * O and lse it stores, for every query and key block, log2 of the query's
+ * unnormalised probability sum over the block (in the workspace); one
+ * reduction with lse turns these into the masses.  The whole step costs one
+ * dense attention plus a pass over 4 bytes per (query, key block), where the
+ * separate calls would cost a dense attention plus the calibration's sweeps
+ * over Q K^T.  o equals losa_sparse_attn_fwd over a full support bitwise;
+ * mass and lse agree with losa_calibrate_mass to fp32 rounding.
  * f32 runs losa_calibrate_mass and a dense fp32 forward.
  */
 losa_status losa_construct(const void* q, const void* k, const void* v, losa_dtype dtype, int B,
@@ -208,10 +224,12 @@ losa_status losa_construct(const void* q, const void* k, const void* v, losa_dty
                            void* stream);
 
 /*
- * Workspace bytes needed by: which = 0 losa_calibrate_mass, 1 losa_select_blocks
- * and losa_select_blocks_topk, 2 losa_sparse_attn_fwd, 3 losa_block_recall,
- * 4 losa_construct (with lse NULL; with lse given, which = 2 suffices).
- * Returns 0 for invalid arguments (then the call itself reports the error).
+ * Workspace bytes needed by: which = 0 losa_calibrate_mass (bf16: the suggested
+ * size of its optional workspace), 1 losa_select_blocks and
+ * losa_select_blocks_topk, 2 losa_sparse_attn_fwd, 3 losa_block_recall,
+ * 4 losa_construct (the suggested size; the least it accepts is the value
+ * for B = H = 1).  Returns 0 for invalid arguments (then the call itself
+ * reports the error).
  */
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
                             int block_k);

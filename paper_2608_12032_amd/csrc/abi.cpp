@@ -82,6 +82,40 @@ size_t elem_bytes(losa_dtype dt) { return dt == LOSA_DTYPE_BF16 ? 2 : 4; }
 
 constexpr size_t kMaxLds = 160 * 1024;
 
+// Workspace of the one-sweep bf16 calibration and of the bf16 construction
+// step for a group of G heads: the block statistics, the heads' lse, then
+// (construction only) the dense forward's V^T.  Heads are processed G at a
+// time; G follows from the bytes the caller gives.
+constexpr size_t kStatGroupCap = (size_t)4 << 30;  // suggested size: up to 4 GiB of groups
+
+size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+struct StatLayout {
+  size_t lse, fwd, total;  // byte offsets of lse and V^T (statistics at 0), total size
+};
+
+StatLayout stat_layout(const Shape& s, int G, bool with_fwd) {
+  StatLayout L;
+  L.lse = up256((size_t)G * losa::stat_bytes_per_head(s.n_pad, s.bk));
+  L.fwd = L.lse + up256((size_t)G * s.n_pad * sizeof(float));
+  L.total = L.fwd + (with_fwd ? up256(losa::sparse_fwd_bf16_workspace(1, G, s.n_pad, s.d, s.n_q))
+                              : 0);
+  return L;
+}
+
+// bytes for one head; a workspace of x bytes holds min(B*H, x / this) heads
+size_t stat_bytes_one_head(const Shape& s, bool with_fwd) {
+  return stat_layout(s, 1, with_fwd).total;
+}
+
+size_t stat_bytes_suggested(const Shape& s, bool with_fwd) {
+  const size_t one = stat_bytes_one_head(s, with_fwd);
+  const int64_t BH = (int64_t)s.B * s.H;
+  int64_t G = (int64_t)(kStatGroupCap / one);
+  G = G < 1 ? 1 : (G > BH ? BH : G);
+  return (size_t)G * one;
+}
+
 }  // namespace
 
 extern "C" {
@@ -90,8 +124,6 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
                                 int N, int d, int block_q, int block_k, float scale, float* mass,
                                 float* lse, void* workspace, size_t workspace_bytes,
                                 void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (!q || !k || !mass) return fail(LOSA_ERR_NULL_POINTER, "q, k and mass must be non-NULL");
   Shape s;
   losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
@@ -103,13 +135,38 @@ losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, 
   st = check_supported(dtype, s);
   if (st != LOSA_OK) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (dtype == LOSA_DTYPE_BF16 && workspace != nullptr) {
+    // one sweep over the keys writing block statistics, a group of heads at a time
+    if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
+    const size_t one = stat_bytes_one_head(s, false);
+    if (workspace_bytes < one)
+      return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu (one head; NULL for no workspace)",
+                  workspace_bytes, one);
+    const int BH = B * H;
+    const int G = (int)((size_t)BH < workspace_bytes / one ? (size_t)BH : workspace_bytes / one);
+    const StatLayout L = stat_layout(s, G, false);
+    char* ws = static_cast<char*>(workspace);
+    const size_t head_bytes = (size_t)s.n_pad * d * 2;
+    for (int bh0 = 0; bh0 < BH; bh0 += G) {
+      const int g = BH - bh0 < G ? BH - bh0 : G;
+      float* l = lse ? lse + (size_t)bh0 * s.n_pad : reinterpret_cast<float*>(ws + L.lse);
+      st = hip_status(losa::launch_calibrate_bf16(
+                          d, block_q, block_k, static_cast<const char*>(q) + bh0 * head_bytes,
+                          static_cast<const char*>(k) + bh0 * head_bytes, 1, g, N, s.n_pad, scale,
+                          mass + (size_t)bh0 * s.n_q * s.n_k, l, reinterpret_cast<float*>(ws), hs),
+                      "losa_calibrate_mass");
+      if (st != LOSA_OK) return st;
+    }
+    return LOSA_OK;
+  }
   if (dtype == LOSA_DTYPE_BF16) {
+    // no workspace: two sweeps over the keys
     if (losa::calib_bf16_lds_bytes(d, block_q, s.n_k) > kMaxLds)
       return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks exceed the calibration LDS budget",
                   s.n_k);
     return hip_status(
         losa::launch_calibrate_bf16(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale, mass, lse,
-                                    false, hs),
+                                    nullptr, hs),
         "losa_calibrate_mass");
   }
   return hip_status(
@@ -272,24 +329,37 @@ losa_status losa_construct(const void* q, const void* k, const void* v, losa_dty
                                                   scale, nullptr, nullptr, 0, o, nullptr, hs),
                       "losa_construct");
   }
-  if (losa::calib_bf16_lds_bytes(d, block_q, s.n_k) > kMaxLds)
-    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks exceed the calibration LDS budget",
-                s.n_k);
-  const size_t fwd_ws = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q);
-  const size_t lse_off = (fwd_ws + 255) / 256 * 256;
-  const size_t need = lse ? fwd_ws : lse_off + (size_t)B * H * s.n_pad * sizeof(float);
-  if (!workspace) return fail(LOSA_ERR_NULL_POINTER, "bf16 needs a workspace of %zu bytes", need);
+  // bf16: the dense forward writes O, lse and the block statistics; the masses
+  // follow from one reduction.  A group of heads at a time.
+  const size_t one = stat_bytes_one_head(s, true);
+  if (!workspace) return fail(LOSA_ERR_NULL_POINTER, "bf16 needs a workspace of >= %zu bytes", one);
   if (!aligned16(workspace)) return fail(LOSA_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
-  if (workspace_bytes < need)
-    return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu", workspace_bytes, need);
-  float* l = lse ? lse : reinterpret_cast<float*>(static_cast<char*>(workspace) + lse_off);
-  st = hip_status(losa::launch_dense_bf16(d, block_q, block_k, q, k, v, B, H, N, s.n_pad, scale, o,
-                                          l, workspace, hs),
-                  "losa_construct (dense attention)");
-  if (st != LOSA_OK) return st;
-  return hip_status(losa::launch_calibrate_bf16(d, block_q, block_k, q, k, B, H, N, s.n_pad, scale,
-                                                mass, l, true, hs),
+  if (workspace_bytes < one)
+    return fail(LOSA_ERR_CAPACITY, "workspace_bytes=%zu < %zu (one head)", workspace_bytes, one);
+  const int BH = B * H;
+  const int G = (int)((size_t)BH < workspace_bytes / one ? (size_t)BH : workspace_bytes / one);
+  const StatLayout L = stat_layout(s, G, true);
+  char* ws = static_cast<char*>(workspace);
+  float* stat = reinterpret_cast<float*>(ws);
+  const size_t head_bytes = (size_t)s.n_pad * d * 2;
+  for (int bh0 = 0; bh0 < BH; bh0 += G) {
+    const int g = BH - bh0 < G ? BH - bh0 : G;
+    const size_t off = bh0 * head_bytes;
+    float* l = lse ? lse + (size_t)bh0 * s.n_pad : reinterpret_cast<float*>(ws + L.lse);
+    st = hip_status(losa::launch_dense_bf16(d, block_q, block_k,
+                                            static_cast<const char*>(q) + off,
+                                            static_cast<const char*>(k) + off,
+                                            static_cast<const char*>(v) + off, 1, g, N, s.n_pad,
+                                            scale, static_cast<char*>(o) + off, l, stat,
+                                            ws + L.fwd, hs),
+                    "losa_construct (dense attention)");
+    if (st != LOSA_OK) return st;
+    st = hip_status(losa::launch_stat_mass(block_q, block_k, stat, l, g, N, s.n_pad,
+                                           mass + (size_t)bh0 * s.n_q * s.n_k, hs),
                     "losa_construct (block masses)");
+    if (st != LOSA_OK) return st;
+  }
+  return LOSA_OK;
 }
 
 size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, int d, int block_q,
@@ -298,19 +368,16 @@ size_t losa_workspace_bytes(int which, losa_dtype dtype, int B, int H, int N, in
   if (check_shape(B, H, N, (which == 1 || which == 3) ? 1 : d, block_q, block_k, &s) != LOSA_OK)
     return 0;
   switch (which) {
-    case 0:
-      return 0;
+    case 0:  // losa_calibrate_mass: optional for bf16 (NULL = two sweeps), unused for fp32
+      return dtype == LOSA_DTYPE_BF16 ? stat_bytes_suggested(s, false) : 0;
     case 1:
       return losa::select_workspace_bytes((int)s.rows, s.n_k);
     case 2:
       return dtype == LOSA_DTYPE_BF16 ? losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) : 0;
     case 3:
       return losa::recall_workspace_bytes((int)s.rows);
-    case 4:  // losa_construct, lse not passed (the larger of the two)
-      return dtype == LOSA_DTYPE_BF16
-                 ? (losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q) + 255) / 256 * 256 +
-                       (size_t)B * H * s.n_pad * sizeof(float)
-                 : 0;
+    case 4:  // losa_construct
+      return dtype == LOSA_DTYPE_BF16 ? stat_bytes_suggested(s, true) : 0;
     default:
       return 0;
   }

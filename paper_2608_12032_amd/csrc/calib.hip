@@ -9,20 +9,32 @@
 // paper's rectangular setting with 128-row query blocks and 32-key key blocks);
 // the keys stream through LDS in tiles of BLK keys either way.
 //
-// The normaliser lse_q is known only after all keys are seen, so a workgroup
-// (one query block, BLK/32 waves of 32 query rows) makes two sweeps over the
-// key tiles of its head:
+// The normaliser lse_q is known only after all keys are seen.  Two schemes:
+//
+// Two sweeps (no workspace): a workgroup (one query block, BLK/32 waves of 32
+// query rows) sweeps the key tiles of its head twice:
 //   1. S^T = K Q^T per tile, running max and running sum -> lse_q (log2
 //      domain) per query, kept in registers;
 //   2. S^T again (identical MFMA order, so identical scores), p = exp2(x -
 //      lse2_q), summed per lane, then across the wave; each wave parks its
 //      per-tile partial in LDS and the workgroup adds the waves' partials in a
 //      fixed order at the end.  No atomics: the result is bitwise repeatable.
+//
+// One sweep with block statistics (STATS): sweep 1 alone, and for every
+// query q and key block j it also stores
+//   a(q, j) = log2( sum_{k in B_j, k < N} 2^(x_qk - m) ) + m,
+// m being the reference the running sum used when block j went by.  a(q, j)
+// is log2 of the block's unnormalised probability sum, so once lse2_q is
+// known, mbar(i, j) = (1 / R_i) sum_q 2^(a(q, j) - lse2_q): stat_mass_kernel
+// does that reduction.  The statistics cost 4 bytes per (query, key block),
+// written once and read once, in place of a second pass of Q K^T and its
+// exponentials.  The dense forward of the construction step writes the same
+// statistics (sparse_fwd.hip), so its masses come from the same reduction.
+//
 // The MFMA orientation is the one of the sparse forward (one query per lane in
 // the S^T accumulator), so the scores are bitwise those the forward computes.
 // K tiles are double-buffered in LDS with direct 16-byte loads; one barrier per
-// tile.  With LSE_IN the normaliser comes from the caller (the dense forward of
-// the construction step already produced it) and only sweep 2 runs.
+// tile.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -79,11 +91,12 @@ __device__ __forceinline__ void tile_scores(const char* buf, const bf16x8_t* qre
   }
 }
 
-template <int D, int BLK, int BK, bool LSE_IN>
+template <int D, int BLK, int BK, bool STATS>
 __global__ void __launch_bounds__(BLK * 2, 2)
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
-                      float* __restrict__ mass, float* __restrict__ lse, int rows_total, int n_q,
-                      int n_k, int N, int n_pad, float scale_log2) {
+                      float* __restrict__ mass, float* __restrict__ lse,
+                      float* __restrict__ stat, int rows_total, int n_q, int n_k, int N,
+                      int n_pad, float scale_log2) {
   using C = CalCfg<D, BLK>;
   static_assert(BK % 32 == 0 && BLK % BK == 0, "key blocks split a tile into whole sub-blocks");
   constexpr int TB = BLK / BK;   // key blocks per tile
@@ -106,9 +119,10 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   const int rows_valid = min(BLK, N - i * BLK);
   float* mrow = mass + (size_t)r * n_k;
 
-  if (rows_valid <= 0) {  // a query block made only of padding
-    for (int j = tid; j < n_k; j += C::NT) mrow[j] = 0.f;
-    if (!LSE_IN && lse != nullptr)
+  if (rows_valid <= 0) {  // a query block made only of padding (STATS: stat_mass zeroes the row)
+    if (!STATS)
+      for (int j = tid; j < n_k; j += C::NT) mrow[j] = 0.f;
+    if (lse != nullptr)
       for (int t = tid; t < BLK; t += C::NT) lse[(size_t)bh * n_pad + i * BLK + t] = -INFINITY;
     return;
   }
@@ -124,19 +138,25 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   const int n_kv = (N + BLK - 1) / BLK;  // key tiles holding a real key
 
   const bool qvalid = qrow < N;
-  float lse2;
-  if constexpr (LSE_IN) {
-    lse2 = qvalid ? lse[(size_t)bh * n_pad + qrow] * kLog2e : 0.f;
-  } else {
   // ---- sweep 1: running max / sum -> lse (log2 units) ----------------------
   float m_run = kNegBig;
   float l_run = 0.f;
+  float pend[TB];  // STATS: the previous tile's block statistics, stored one tile late
   issue_tile<D, BLK>(buf0, krs, 0, w, lane);
   for (int j = 0; j < n_kv; ++j) {
     char* cur = (j & 1) ? buf1 : buf0;
     char* nxt = (j & 1) ? buf0 : buf1;
     wait_vm_barrier<0>();  // tile j landed; every wave is done with tile j-1
     if (j + 1 < n_kv) issue_tile<D, BLK>(nxt, krs, j + 1, w, lane);
+    if constexpr (STATS) {
+      // the stores go out a whole tile before the next vmcnt(0) wait, which
+      // then finds them done instead of waiting out their latency
+      if (j > 0 && g == 0) {
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+          stat[((size_t)bh * n_k + (j - 1) * TB + b) * n_pad + qrow] = pend[b];
+      }
+    }
     f32x16_t sacc[C::KB];
     tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
@@ -151,19 +171,36 @@ __global__ void __launch_bounds__(BLK * 2, 2)
         mx = fmaxf(mx, x);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float lsum = 0.f;
+    float bs[TB];  // this lane's sum per key block of the tile
+#pragma unroll
+    for (int b = 0; b < TB; ++b) bs[b] = 0.f;
 #pragma unroll
     for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-      for (int t = 0; t < 16; ++t) lsum += fast_exp2(sacc[kb][t] - mx);
+      for (int t = 0; t < 16; ++t) bs[kb / SPB] += fast_exp2(sacc[kb][t] - mx);
+    float lsum = 0.f;
+#pragma unroll
+    for (int b = 0; b < TB; ++b) lsum += bs[b];
     l_run = l_run * fast_exp2(m_run - mx) + lsum;
     m_run = mx;
+    if constexpr (STATS) {
+#pragma unroll
+      for (int b = 0; b < TB; ++b) pend[b] = __log2f(bs[b] + __shfl_xor(bs[b], 32)) + mx;
+    }
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  lse2 = m_run + __log2f(l_tot);
+  const float lse2 = m_run + __log2f(l_tot);
   if (lse != nullptr && g == 0)
     lse[(size_t)bh * n_pad + qrow] = qvalid ? lse2 * kLn2 : -INFINITY;
+  if constexpr (STATS) {
+    if (g == 0) {
+#pragma unroll
+      for (int b = 0; b < TB; ++b)
+        stat[((size_t)bh * n_k + (n_kv - 1) * TB + b) * n_pad + qrow] = pend[b];
+    }
+    return;
   }
+
   // padding rows contribute exp2(x - inf) = 0 to every mass
   const float sub = qvalid ? lse2 : INFINITY;
 
@@ -208,25 +245,115 @@ __global__ void __launch_bounds__(BLK * 2, 2)
   }
 }
 
-template <int D, int BLK, int BK, bool LSE_IN>
+// mbar(i, j) = (1 / R_i) sum_{q in B_i, q < N} 2^(a(q, j) - lse2_q) from the
+// block statistics a [BH][n_k][n_pad] (log2 units) and the natural-log
+// normalisers lse [BH][n_pad].  One workgroup per mass row (bh, i); wave w
+// takes groups of kStatGroup consecutive key blocks, each lane QPL adjacent
+// queries of block i, so a wave reads BLK contiguous floats per key block and
+// has kStatGroup such reads in flight.  Lanes 0..kStatGroup-1 then store the
+// group's masses with one contiguous store.  Key blocks j >= n_kb hold no
+// valid key and rows made only of padding get 0; padding queries are never
+// read into the sum.  Fixed summation order: bitwise repeatable.
+constexpr int kStatT = 256;
+constexpr int kStatGroup = 8;
+
+template <int BLK>
+__global__ void __launch_bounds__(kStatT)
+    stat_mass_kernel(const float* __restrict__ stat, const float* __restrict__ lse, int n_q,
+                     int n_k, int n_kb, int N, int n_pad, float* __restrict__ mass) {
+  constexpr int QPL = BLK / 64;
+  constexpr int NWV = kStatT / 64;
+  static_assert(QPL == 1 || QPL == 2, "64- or 128-row query blocks");
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int r = blockIdx.x;
+  const int bh = r / n_q;
+  const int i = r - bh * n_q;
+  float* mrow = mass + (size_t)r * n_k;
+  const int rows_valid = min(BLK, N - i * BLK);
+  if (rows_valid <= 0) {
+    for (int j = threadIdx.x; j < n_k; j += kStatT) mrow[j] = 0.f;
+    return;
+  }
+  const int q0 = i * BLK + lane * QPL;
+  bool ok[QPL];
+  float sub[QPL];
+#pragma unroll
+  for (int e = 0; e < QPL; ++e) {
+    ok[e] = q0 + e < N;
+    sub[e] = ok[e] ? lse[(size_t)bh * n_pad + q0 + e] * kLog2e : 0.f;
+  }
+  const float inv = 1.0f / (float)rows_valid;
+  const float* base = stat + (size_t)bh * n_k * n_pad + q0;
+  for (int j0 = w * kStatGroup; j0 < n_k; j0 += NWV * kStatGroup) {
+    float v[kStatGroup][QPL];
+#pragma unroll
+    for (int u = 0; u < kStatGroup; ++u) {
+      const int j = j0 + u;
+      if (j < n_kb) {
+        const float* src = base + (size_t)j * n_pad;
+        if constexpr (QPL == 2) {
+          const f32x2_t t = *reinterpret_cast<const f32x2_t*>(src);
+          v[u][0] = t[0];
+          v[u][1] = t[1];
+        } else {
+          v[u][0] = *src;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < QPL; ++e) v[u][e] = 0.f;
+      }
+    }
+    float mine = 0.f;
+#pragma unroll
+    for (int u = 0; u < kStatGroup; ++u) {
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < QPL; ++e) acc += ok[e] ? fast_exp2(v[u][e] - sub[e]) : 0.f;
+      acc = wave_sum(acc);
+      if (lane == u) mine = (j0 + u < n_kb) ? acc * inv : 0.f;
+    }
+    if (lane < kStatGroup && j0 + lane < n_k) mrow[j0 + lane] = mine;
+  }
+}
+
+template <int D, int BLK, int BK, bool STATS>
 hipError_t launch_cal(const void* q, const void* k, int B, int H, int N, int n_pad, float scale,
-                      float* mass, float* lse, hipStream_t stream) {
+                      float* mass, float* lse, float* stat, hipStream_t stream) {
   using C = CalCfg<D, BLK>;
   const int n_q = n_pad / BLK;
   const int n_k = n_pad / BK;
   const int rows = B * H * n_q;
-  const size_t lds = 2 * (size_t)C::TILE + (size_t)C::NW * n_k * sizeof(float);
+  const size_t lds = 2 * (size_t)C::TILE + (STATS ? 0 : (size_t)C::NW * n_k * sizeof(float));
   hipError_t err =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK, BK, LSE_IN>),
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&calib_bf16_kernel<D, BLK, BK, STATS>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK, BK, LSE_IN>), dim3(rows), dim3(C::NT), lds, stream,
+  hipLaunchKernelGGL((calib_bf16_kernel<D, BLK, BK, STATS>), dim3(rows), dim3(C::NT), lds, stream,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), mass, lse,
-                     rows, n_q, n_k, N, n_pad, scale * kLog2e);
-  return hipGetLastError();
+                     stat, rows, n_q, n_k, N, n_pad, scale * kLog2e);
+  err = hipGetLastError();
+  if (err != hipSuccess || !STATS) return err;
+  return launch_stat_mass(BLK, BK, stat, lse, B * H, N, n_pad, mass, stream);
 }
 
 }  // namespace
+
+hipError_t launch_stat_mass(int blk, int blk_k, const float* stat, const float* lse, int BH, int N,
+                            int n_pad, float* mass, hipStream_t stream) {
+  const int n_q = n_pad / blk;
+  const int n_k = n_pad / blk_k;
+  const int n_kb = (N + blk_k - 1) / blk_k;
+  if (blk == 128)
+    hipLaunchKernelGGL(stat_mass_kernel<128>, dim3(BH * n_q), dim3(kStatT), 0, stream, stat, lse,
+                       n_q, n_k, n_kb, N, n_pad, mass);
+  else if (blk == 64)
+    hipLaunchKernelGGL(stat_mass_kernel<64>, dim3(BH * n_q), dim3(kStatT), 0, stream, stat, lse,
+                       n_q, n_k, n_kb, N, n_pad, mass);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 size_t calib_bf16_lds_bytes(int d, int blk, int n_k) {
   return 2 * (size_t)blk * d * 2 + (size_t)(blk / 32) * n_k * sizeof(float);
@@ -234,11 +361,13 @@ size_t calib_bf16_lds_bytes(int d, int blk, int n_k) {
 
 hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                  int H, int N, int n_pad, float scale, float* mass, float* lse,
-                                 bool lse_in, hipStream_t stream) {
-#define LOSA_CAL(DD, BB, KK)                                                              \
-  if (d == DD && blk == BB && blk_k == KK)                                                \
-    return lse_in ? launch_cal<DD, BB, KK, true>(q, k, B, H, N, n_pad, scale, mass, lse, stream) \
-                  : launch_cal<DD, BB, KK, false>(q, k, B, H, N, n_pad, scale, mass, lse, stream);
+                                 float* stat, hipStream_t stream) {
+#define LOSA_CAL(DD, BB, KK)                                                                 \
+  if (d == DD && blk == BB && blk_k == KK)                                                   \
+    return stat ? launch_cal<DD, BB, KK, true>(q, k, B, H, N, n_pad, scale, mass, lse, stat,  \
+                                                stream)                                      \
+                : launch_cal<DD, BB, KK, false>(q, k, B, H, N, n_pad, scale, mass, lse, nullptr, \
+                                                 stream);
   LOSA_CAL(128, 128, 128)
   LOSA_CAL(64, 128, 128)
   LOSA_CAL(128, 64, 64)

@@ -16,11 +16,18 @@ __host__ __device__ inline int padded_len(int N, int block_q, int block_k) {
 }
 
 // blk = query block rows, blk_k = key block keys (blk, or 32)
-// lse_in: lse holds the natural-log normalisers already (from the dense
-// forward of the construction step) and only the mass sweep runs
+// stat == nullptr: two sweeps over the keys, lse optional.
+// stat != nullptr: one sweep that writes the block statistics
+//   [B*H][n_k][n_pad] fp32 and lse (then required), then launch_stat_mass.
 hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                  int H, int N, int n_pad, float scale, float* mass, float* lse,
-                                 bool lse_in, hipStream_t stream);
+                                 float* stat, hipStream_t stream);
+// Block masses [BH][n_q][n_k] from block statistics and natural-log lse.
+hipError_t launch_stat_mass(int blk, int blk_k, const float* stat, const float* lse, int BH, int N,
+                            int n_pad, float* mass, hipStream_t stream);
+inline size_t stat_bytes_per_head(int n_pad, int blk_k) {
+  return (size_t)(n_pad / blk_k) * n_pad * sizeof(float);
+}
 hipError_t launch_calibrate_f32(int d, int blk, int blk_k, const void* q, const void* k, int B,
                                 int H, int N, int n_pad, float scale, float* mass, float* lse,
                                 hipStream_t stream);
@@ -39,9 +46,10 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, cons
                                   int64_t col_len, void* o, float* lse, void* workspace,
                                   hipStream_t stream);
 // dense attention over every valid key (row_ptr == nullptr for the f32 path)
+// stat != nullptr: also the block statistics [B*H][n_k][n_pad] (log2 units)
 hipError_t launch_dense_bf16(int d, int blk, int blk_k, const void* q, const void* k,
                              const void* v, int B, int H, int N, int n_pad, float scale, void* o,
-                             float* lse, void* workspace, hipStream_t stream);
+                             float* lse, float* stat, void* workspace, hipStream_t stream);
 hipError_t launch_sparse_fwd_f32(int d, int blk, int blk_k, const void* q, const void* k,
                                  const void* v, int B, int H, int N, int n_pad, float scale,
                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_len,

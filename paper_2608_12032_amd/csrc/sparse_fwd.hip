@@ -310,15 +310,15 @@ __device__ __forceinline__ void mask_sub(f32x16_t& s, int part, int kvalid, int 
 // (at most 2^20 per key over at most 2^19 keys).
 constexpr float kSumBound = 1048576.0f;
 
-template <int D, int BLK, int BK>
+template <int D, int BLK, int BK, bool DENSE>
 __global__ void __launch_bounds__(BLK * 2)
     __attribute__((amdgpu_waves_per_eu(BLK == 128 ? 2 : 1)))
     sparse_fwd_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                            const __bf16* __restrict__ Vt, const int32_t* __restrict__ row_ptr,
                            const int32_t* __restrict__ col_idx, int64_t col_len,
                            __bf16* __restrict__ O, float* __restrict__ lse,
-                           const int* __restrict__ order, int n_q, int n_k, int N, int n_pad,
-                           float scale_log2, int dense) {
+                           float* __restrict__ bstat, const int* __restrict__ order, int n_q,
+                           int n_k, int N, int n_pad, float scale_log2) {
   using C = FwdCfg<D, BLK, BK>;
   constexpr int NS = C::NS;
   constexpr int R = C::R;
@@ -333,10 +333,11 @@ __global__ void __launch_bounds__(BLK * 2)
   const int l32 = lane & 31;
   const int g = lane >> 5;
 
-  // dense: every row keeps every key block that holds a valid key (the dense
+  // DENSE: every row keeps every key block that holds a valid key (the dense
   // attention of the construction step); rows run in id order, each XCD on a
-  // contiguous range of them
-  const int r = dense ? xcd_remap(blockIdx.x, gridDim.x) : order[blockIdx.x];
+  // contiguous range of them.  A template flag, so that the two modes are
+  // separate kernels in a trace.
+  const int r = DENSE ? xcd_remap(blockIdx.x, gridDim.x) : order[blockIdx.x];
   const int bh = r / n_q;
   const int qb = r - bh * n_q;
   const size_t head = (size_t)bh * n_pad * D;
@@ -347,7 +348,7 @@ __global__ void __launch_bounds__(BLK * 2)
   // ---- the row's distinct valid key blocks, ascending ---------------------
   // (flags and per-wave counts live in the rings, unused until the first load)
   int nb = 0;
-  if (dense) {
+  if constexpr (DENSE) {
     nb = (N + BK - 1) / BK;
     for (int j = tid; j < nb; j += C::NT) list[j] = (uint16_t)j;
     __syncthreads();
@@ -446,6 +447,7 @@ __global__ void __launch_bounds__(BLK * 2)
   for (int db = 0; db < C::DB; ++db) oacc[db] = f32x16_t{};
   float m_run = kNegBig;  // max used for exp2 (scaled units)
   float l_run = 0.f;      // this lane's share of the row sum
+  float b_run = 0.f;      // DENSE: this lane's share of the current key block's sum
   f32x16_t sc[2];         // raw scores of the sub-tiles with even / odd index
   bf16x8_t pb[2][2];      // bf16 probabilities of the sub-tiles with even / odd index
 
@@ -529,11 +531,24 @@ __global__ void __launch_bounds__(BLK * 2)
         const float alpha = fast_exp2(m_run - m_new);
         m_run = m_new;
         l_run *= alpha;
+        if constexpr (DENSE) b_run *= alpha;
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) oacc[db] *= alpha;
         ls = softmax_sub(cur, scale_log2, m_run, pb[H & 1]);
       }
       l_run += ls;
+      if constexpr (DENSE) {
+        // block statistic of the construction step: log2 of the query's
+        // unnormalised probability sum over key block jc[H / NS] (its last
+        // sub-tile is s), in absolute units, for the block-mass reduction
+        b_run += ls;
+        if constexpr (H % NS == NS - 1) {
+          const float bt = add_partner(b_run);
+          b_run = 0.f;
+          if (bstat != nullptr && s < S_real && g == 0)
+            bstat[((size_t)bh * n_k + jc[H / NS]) * n_pad + qrow] = __log2f(bt) + m_run;
+        }
+      }
     };
 
     using I0 = std::integral_constant<int, 0>;
@@ -695,18 +710,20 @@ hipError_t launch_fwd(const void* q, const void* k, const void* v, int B, int H,
   dim3 tgrid(n_pad / 64, BH);
   hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
                      static_cast<const __bf16*>(v), vt, n_pad);
-  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(FwdCfg<D, BLK, BK>::NT), 0,
-                     stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
-                     static_cast<const __bf16*>(vt), row_ptr, col_idx, col_len,
-                     static_cast<__bf16*>(o), lse, order, n_q, n_k, N, n_pad, scale * kLog2e, 0);
+  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK, false>), dim3(rows),
+                     dim3(FwdCfg<D, BLK, BK>::NT), 0, stream, static_cast<const __bf16*>(q),
+                     static_cast<const __bf16*>(k), static_cast<const __bf16*>(vt), row_ptr,
+                     col_idx, col_len, static_cast<__bf16*>(o), lse, nullptr, order, n_q, n_k, N,
+                     n_pad, scale * kLog2e);
   return hipGetLastError();
 }
 
 // Dense attention of every query block over every valid key (the forward
-// kernel with full rows): O and lse of the construction step.
+// kernel with full rows): O, lse and, if stat is given, the block statistics
+// of the construction step.
 template <int D, int BLK, int BK>
 hipError_t launch_dense(const void* q, const void* k, const void* v, int B, int H, int N,
-                        int n_pad, float scale, void* o, float* lse, void* workspace,
+                        int n_pad, float scale, void* o, float* lse, float* stat, void* workspace,
                         hipStream_t stream) {
   const int BH = B * H;
   const int n_q = n_pad / BLK;
@@ -716,10 +733,11 @@ hipError_t launch_dense(const void* q, const void* k, const void* v, int B, int 
   dim3 tgrid(n_pad / 64, BH);
   hipLaunchKernelGGL(transpose_v_kernel<D>, tgrid, dim3(256), 0, stream,
                      static_cast<const __bf16*>(v), vt, n_pad);
-  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK>), dim3(rows), dim3(FwdCfg<D, BLK, BK>::NT),
-                     0, stream, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
-                     static_cast<const __bf16*>(vt), nullptr, nullptr, 0, static_cast<__bf16*>(o),
-                     lse, nullptr, n_q, n_k, N, n_pad, scale * kLog2e, 1);
+  hipLaunchKernelGGL((sparse_fwd_bf16_kernel<D, BLK, BK, true>), dim3(rows),
+                     dim3(FwdCfg<D, BLK, BK>::NT), 0, stream, static_cast<const __bf16*>(q),
+                     static_cast<const __bf16*>(k), static_cast<const __bf16*>(vt), nullptr,
+                     nullptr, 0, static_cast<__bf16*>(o), lse, stat, nullptr, n_q, n_k, N, n_pad,
+                     scale * kLog2e);
   return hipGetLastError();
 }
 
@@ -748,10 +766,11 @@ hipError_t launch_sparse_fwd_bf16(int d, int blk, int blk_k, const void* q, cons
 
 hipError_t launch_dense_bf16(int d, int blk, int blk_k, const void* q, const void* k,
                              const void* v, int B, int H, int N, int n_pad, float scale, void* o,
-                             float* lse, void* workspace, hipStream_t stream) {
-#define LOSA_DENSE(DD, BB, KK)                                                                 \
-  if (d == DD && blk == BB && blk_k == KK)                                                     \
-    return launch_dense<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, o, lse, workspace, stream);
+                             float* lse, float* stat, void* workspace, hipStream_t stream) {
+#define LOSA_DENSE(DD, BB, KK)                                                                \
+  if (d == DD && blk == BB && blk_k == KK)                                                    \
+    return launch_dense<DD, BB, KK>(q, k, v, B, H, N, n_pad, scale, o, lse, stat, workspace, \
+                                    stream);
   LOSA_DENSE(128, 128, 128)
   LOSA_DENSE(64, 128, 128)
   LOSA_DENSE(128, 64, 64)

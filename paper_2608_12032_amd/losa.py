@@ -101,8 +101,14 @@ def workspace_bytes(which: int, dtype_code: int, B, H, N, d, block_q, block_k) -
 
 
 def losa_calibrate_mass(q, k, N: int, block_q: int, block_k: int | None = None,
-                        scale: float | None = None, want_lse: bool = True, mass=None, lse=None):
-    """Exact block masses of a dense step -> (mass [B,H,n_q,n_k] fp32, lse or None)."""
+                        scale: float | None = None, want_lse: bool = True, mass=None, lse=None,
+                        workspace=None, two_sweep: bool = False):
+    """Exact block masses of a dense step -> (mass [B,H,n_q,n_k] fp32, lse or None).
+
+    bf16 takes one sweep over the keys plus a reduction of per-(query, key
+    block) statistics held in ``workspace`` (allocated at the suggested size
+    when not given); ``two_sweep=True`` passes no workspace and takes two
+    sweeps instead."""
     block_k = block_k or block_q
     B, H, Np, d = _qkv_shape(q)
     if k.shape != q.shape or k.dtype != q.dtype:
@@ -115,8 +121,16 @@ def losa_calibrate_mass(q, k, N: int, block_q: int, block_k: int | None = None,
         lse = torch.empty((B, H, Np), dtype=torch.float32, device=q.device)
     if not want_lse:
         lse = None
-    st = lib.losa_calibrate_mass(_ptr(q), _ptr(k), _dtype_code(q), B, H, N, d, block_q, block_k,
-                                 scale, _ptr(mass), _ptr(lse), None, 0, _stream(q.device))
+    dcode = _dtype_code(q)
+    if two_sweep or dcode != LOSA_DTYPE_BF16:
+        workspace = None
+    elif workspace is None:
+        need = workspace_bytes(0, dcode, B, H, N, d, block_q, block_k)
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.losa_calibrate_mass(_ptr(q), _ptr(k), dcode, B, H, N, d, block_q, block_k,
+                                 scale, _ptr(mass), _ptr(lse), _ptr(workspace), ws_bytes,
+                                 _stream(q.device))
     _check(st, "losa_calibrate_mass")
     return mass, lse
 
@@ -235,7 +249,7 @@ def losa_construct(q, k, v, N: int, block_q: int, block_k: int | None = None,
         lse = torch.empty((B, H, Np), dtype=torch.float32, device=q.device)
     if not want_lse:
         lse = None
-    need = workspace_bytes(4 if lse is None else 2, dcode, B, H, N, d, block_q, block_k)
+    need = workspace_bytes(4, dcode, B, H, N, d, block_q, block_k)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()

@@ -47,8 +47,8 @@ MIS = 0x10001           # misaligned
 
 
 def _cal(L, q=FAKE, k=FAKE, dtype=1, B=1, H=2, N=1000, d=128, bq=128, bk=128, scale=0.1,
-         mass=FAKE, lse=None):
-    return L.lib.losa_calibrate_mass(q, k, dtype, B, H, N, d, bq, bk, scale, mass, lse, None, 0,
+         mass=FAKE, lse=None, ws=None, wsb=0):
+    return L.lib.losa_calibrate_mass(q, k, dtype, B, H, N, d, bq, bk, scale, mass, lse, ws, wsb,
                                      None)
 
 
@@ -69,6 +69,8 @@ def _fwd(L, q=FAKE, dtype=1, B=1, H=2, N=1000, d=128, bq=128, bk=128, rp=FAKE, c
     (dict(scale=float("nan")), 2), (dict(q=MIS), 4), (dict(lse=MIS), 4),
     (dict(d=96), 5), (dict(bq=128, bk=64), 5), (dict(bq=32, bk=32), 5), (dict(dtype=7), 5),
     (dict(N=1 << 30, d=128), 2),
+    # the optional bf16 workspace: aligned, and at least one head's share
+    (dict(ws=MIS, wsb=10**9), 4), (dict(ws=FAKE, wsb=100), 6),
 ])
 def test_calibrate_validation(L, kw, code):
     assert _cal(L, **kw) == code
@@ -149,14 +151,26 @@ def test_construct_validation(L, kw, code):
 
 def test_workspace_sizes(L):
     B, H, N, d = 1, 12, 32760, 128
-    assert L.workspace_bytes(0, 1, B, H, N, d, 128, 128) == 0
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    stat_head = 256 * 32768 * 4              # one fp32 per (query, key block) of a head
+    one_cal = up(stat_head) + up(32768 * 4)  # statistics, lse
+    assert L.workspace_bytes(0, 1, 1, 1, N, d, 128, 128) == one_cal
+    assert L.workspace_bytes(0, 1, B, H, N, d, 128, 128) == H * one_cal
+    assert L.workspace_bytes(0, 0, B, H, N, d, 128, 128) == 0
+    # 32-key blocks: four times the statistics
+    assert L.workspace_bytes(0, 1, 1, 1, N, d, 128, 32) == up(4 * stat_head) + up(32768 * 4)
+    # the suggestion stops at 4 GiB worth of whole heads
+    big = L.workspace_bytes(0, 1, 1, 200, N, d, 128, 128)
+    assert big == (4 << 30) // one_cal * one_cal
     assert L.workspace_bytes(2, 1, B, H, N, d, 128, 128) == B * H * 32768 * d * 2 + B * H * 256 * 4
     assert L.workspace_bytes(2, 0, B, H, N, d, 128, 128) == 0
     rows, n_k = 12 * 256, 256
     assert L.workspace_bytes(1, 0, B, H, N, 1, 128, 128) == ((rows * 4 + 255) // 256) * 256 + rows * n_k
     assert L.workspace_bytes(3, 0, B, H, N, 1, 128, 128) == rows * 16
-    fwd = L.workspace_bytes(2, 1, B, H, N, d, 128, 128)
-    assert L.workspace_bytes(4, 1, B, H, N, d, 128, 128) == (fwd + 255) // 256 * 256 + H * 32768 * 4
+    one_con = one_cal + up(L.workspace_bytes(2, 1, 1, 1, N, d, 128, 128))  # + V^T and order
+    assert L.workspace_bytes(4, 1, 1, 1, N, d, 128, 128) == one_con
+    assert L.workspace_bytes(4, 1, B, H, N, d, 128, 128) == H * one_con
+    assert L.workspace_bytes(4, 0, B, H, N, d, 128, 128) == 0
     assert L.workspace_bytes(5, 1, B, H, N, d, 128, 128) == 0
     assert L.workspace_bytes(2, 1, 0, H, N, d, 128, 128) == 0
 

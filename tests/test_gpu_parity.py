@@ -361,6 +361,59 @@ def test_fwd_writes_every_row_once(L, key):
     assert mx <= OUT_MAX and mean <= OUT_MEAN, (mx, mean)
 
 
+@pytest.mark.parametrize("key", ["cog-bf16-d64-ragged", "wan-bf16-d128-r128c32", "f32-d64-blk128"])
+def test_padding_contents_are_ignored(L, key):
+    """Rows n >= N of Q, K and V may hold any finite values: with large random
+    values there, every output agrees with the zero-padded run (padded keys
+    are masked before the exponential, padded queries are never read into a
+    mass).  Not bitwise: a padded query row shares its wave with valid rows,
+    and its scores may trigger an earlier softmax rescale of the wave."""
+    w = SMALL[key]
+    N, Cq, Ck = w.N, w.block, w.bk
+    assert N < w.N_pad
+    q, k, v = W.make_inputs(w, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    qg, kg, vg = q.clone(), k.clone(), v.clone()
+    for t in (qg, kg, vg):
+        t[:, :, N:] = (torch.randn(t[:, :, N:].shape, generator=gen, device="cuda") * 300).to(t.dtype)
+
+    def run(q, k, v, fwd_csr=None):
+        m1, l1 = L.losa_calibrate_mass(q, k, N, Cq, Ck)
+        m2, _ = L.losa_calibrate_mass(q, k, N, Cq, Ck, two_sweep=True)
+        rp, ci = L.losa_select_blocks(m1, N, Cq, Ck, w.tau)
+        frp, fci = fwd_csr if fwd_csr is not None else (rp, ci)   # the forward on one support
+        o, lo = L.losa_sparse_attn_fwd(q, k, v, N, Cq, Ck, frp, fci, want_lse=True)
+        oc, mc = L.losa_construct(q, k, v, N, Cq, Ck)
+        torch.cuda.synchronize()
+        return [f64(x) for x in (m1, l1, m2, o, lo, oc, mc)], (rp, ci)
+
+    ref, csr_ref = run(q, k, v)
+    got, csr_got = run(qg, kg, vg, fwd_csr=csr_ref)
+    csr_ref = (csr_ref[0], csr_ref[1][:L.nnz(csr_ref[0])])
+    csr_got = (csr_got[0], csr_got[1][:L.nnz(csr_got[0])])
+    tol = 1e-4 if w.dtype == "f32" else 1e-2
+    for name, a, b, t in zip(("mass", "lse", "mass2", "o", "lse_o", "o_con", "mass_con"), ref, got,
+                             (1e-6, 1e-5, 1e-6, tol, 1e-5, tol, 1e-6)):
+        a, b = a.copy(), b.copy()
+        if name.startswith("lse"):
+            assert np.all(np.isneginf(b[:, :, N:])), name
+            a, b = a[:, :, :N], b[:, :, :N]
+        if name.startswith("o"):
+            assert np.all(b[:, :, N:] == 0), name
+        err = np.abs(a - b).max()
+        say(f"padding {key}: {name} {err:.2e}")
+        assert err <= t, (name, err)
+    if not all(x.shape == y.shape and torch.equal(x, y) for x, y in zip(csr_ref, csr_got)):
+        # a flip is allowed only for blocks within rounding of tau
+        m = ref[0].reshape(-1, w.n_kblocks)
+        details = [O.select_row(m[r], tau32(w.tau), O.num_valid_key_blocks(N, Ck),
+                                (r % w.n_blocks) * Cq < N) for r in range(m.shape[0])]
+        rp_g = csr_got[0].cpu().numpy().astype(np.int64)
+        cmp = CMP.compare_selection(rp_g, csr_got[1].cpu().numpy().astype(np.int64), details, m,
+                                    tau32(w.tau))
+        assert cmp["ok"], cmp
+
+
 def test_deterministic(L):
     w = SMALL["cog-bf16-d64-ragged"]
     q, k, v = W.make_inputs(w, device="cuda")
