@@ -79,7 +79,7 @@ typedef enum { LOSA_DTYPE_F32 = 0, LOSA_DTYPE_BF16 = 1 } losa_dtype;
  *            losa_workspace_bytes(0, dtype, 1, 1, N, d, block_q, block_k);
  *            heads are processed as many at a time as it holds, and
  *            losa_workspace_bytes(0, ...) suggests room for all of them, up to
- *            4 GiB.  Contents on entry are ignored and overwritten.  f32:
+ *            16 GiB.  Contents on entry are ignored and overwritten.  f32:
  *            ignored (two sweeps).
  * Arithmetic: bf16 inputs use bf16 matrix-core products with fp32
  * accumulation; f32 inputs use fp32 throughout.  Both bf16 schemes compute
@@ -207,7 +207,7 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
  *       losa_workspace_bytes(4, dtype, 1, 1, N, d, block_q, block_k); heads
  *       are processed as many at a time as it holds, and
  *       losa_workspace_bytes(4, ...) suggests room for all of them, up to
- *       4 GiB.  f32: unused.
+ *       16 GiB.  f32: unused.
  * bf16 runs the sparse forward's kernel over every valid key block.  Besides
  * O and lse it stores, for every query and key block, log2 of the query's
  * unnormalised probability sum over the block (in the workspace); one

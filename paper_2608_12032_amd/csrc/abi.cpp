@@ -86,7 +86,7 @@ constexpr size_t kMaxLds = 160 * 1024;
 // step for a group of G heads: the block statistics, the heads' lse, then
 // (construction only) the dense forward's V^T.  Heads are processed G at a
 // time; G follows from the bytes the caller gives.
-constexpr size_t kStatGroupCap = (size_t)4 << 30;  // suggested size: up to 4 GiB of groups
+constexpr size_t kStatGroupCap = (size_t)16 << 30;  // suggested size: up to 16 GiB of groups
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 

@@ -159,9 +159,9 @@ def test_workspace_sizes(L):
     assert L.workspace_bytes(0, 0, B, H, N, d, 128, 128) == 0
     # 32-key blocks: four times the statistics
     assert L.workspace_bytes(0, 1, 1, 1, N, d, 128, 32) == up(4 * stat_head) + up(32768 * 4)
-    # the suggestion stops at 4 GiB worth of whole heads
-    big = L.workspace_bytes(0, 1, 1, 200, N, d, 128, 128)
-    assert big == (4 << 30) // one_cal * one_cal
+    # the suggestion stops at 16 GiB worth of whole heads
+    big = L.workspace_bytes(0, 1, 1, 600, N, d, 128, 128)
+    assert big == (16 << 30) // one_cal * one_cal
     assert L.workspace_bytes(2, 1, B, H, N, d, 128, 128) == B * H * 32768 * d * 2 + B * H * 256 * 4
     assert L.workspace_bytes(2, 0, B, H, N, d, 128, 128) == 0
     rows, n_k = 12 * 256, 256
