@@ -91,6 +91,48 @@ __device__ __forceinline__ void tile_scores(const char* buf, const bf16x8_t* qre
   }
 }
 
+// Scores of keys at or beyond kvalid (tile-relative) -> -inf: the ragged last
+// key tile only.
+template <int KB>
+__device__ __forceinline__ void mask_tile(f32x16_t* s, int kvalid, int g) {
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int key = kb * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
+      if (key >= kvalid) s[kb][t] = -INFINITY;
+    }
+}
+
+// This lane's probabilities 2^(c*s - m) of a tile, summed per key block of the
+// tile (bs, TB blocks of SPB 32-key sub-blocks; one partial per sub-block, for
+// independent add chains); returns the lane's tile sum.
+template <int KB, int TB>
+__device__ __forceinline__ float tile_sums(const f32x16_t* s, float c, float m, float* bs) {
+  constexpr int SPB = KB / TB;
+  float acc[KB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    acc[kb] = 0.f;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) acc[kb] += fast_exp2(__builtin_fmaf(s[kb][t], c, -m));
+  }
+  float l = 0.f;
+#pragma unroll
+  for (int b = 0; b < TB; ++b) {
+    bs[b] = acc[b * SPB];
+#pragma unroll
+    for (int u = 1; u < SPB; ++u) bs[b] += acc[b * SPB + u];
+    l += bs[b];
+  }
+  return l;
+}
+
+// Bound on one lane's tile sum (so on each probability) before the running
+// max must be raised: the max used trails the true one by at most 20 (log2
+// units), and l stays far from fp32 overflow (2^20 per key, at most 2^19 keys).
+constexpr float kCalSumBound = 1048576.0f;
+
 template <int D, int BLK, int BK, bool STATS>
 __global__ void __launch_bounds__(BLK * 2, 2)
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
@@ -129,15 +171,17 @@ __global__ void __launch_bounds__(BLK * 2, 2)
 
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(K + head, (uint32_t)((size_t)n_pad * D * 2));
   const int qrow = i * BLK + w * 32 + l32;
+  const bool qvalid = qrow < N;
+  // padding query rows take Q = 0: their scores stay finite whatever the
+  // padding holds, and they are never read into a mass
   bf16x8_t qreg[C::KS];
   {
     const bf16x8_t* qp = reinterpret_cast<const bf16x8_t*>(Q + head + (size_t)qrow * D);
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[s] = qp[2 * s + g];
+    for (int s = 0; s < C::KS; ++s) qreg[s] = qvalid ? qp[2 * s + g] : bf16x8_t{};
   }
   const int n_kv = (N + BLK - 1) / BLK;  // key tiles holding a real key
 
-  const bool qvalid = qrow < N;
   // ---- sweep 1: running max / sum -> lse (log2 units) ----------------------
   float m_run = kNegBig;
   float l_run = 0.f;
@@ -160,32 +204,29 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     f32x16_t sacc[C::KB];
     tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
-    float mx = m_run;
+    if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
+    // Probabilities against the running max, without looking at this tile's
+    // scores first.  If a lane's tile sum exceeds the bound (or is inf: the
+    // first tile), the max is raised to the tile's and the sums redone; both
+    // lanes of a query take the same max, so their sums stay comparable.
+    float bs[TB];
+    float lsum = tile_sums<C::KB, TB>(sacc, scale_log2, m_run, bs);
+    if (__ballot(!(lsum <= kCalSumBound)) != 0) {
+      float mx = sacc[0][0];
 #pragma unroll
-    for (int kb = 0; kb < C::KB; ++kb)
+      for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        const int key = kb * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
-        const float x = key < kvalid ? sacc[kb][t] * scale_log2 : -INFINITY;
-        sacc[kb][t] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float bs[TB];  // this lane's sum per key block of the tile
-#pragma unroll
-    for (int b = 0; b < TB; ++b) bs[b] = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-      for (int t = 0; t < 16; ++t) bs[kb / SPB] += fast_exp2(sacc[kb][t] - mx);
-    float lsum = 0.f;
-#pragma unroll
-    for (int b = 0; b < TB; ++b) lsum += bs[b];
-    l_run = l_run * fast_exp2(m_run - mx) + lsum;
-    m_run = mx;
+        for (int t = 0; t < 16; ++t) mx = fmaxf(mx, sacc[kb][t]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;  // scale > 0: max commutes with it
+      const float m_new = fmaxf(m_run, mx);
+      l_run *= fast_exp2(m_run - m_new);
+      m_run = m_new;
+      lsum = tile_sums<C::KB, TB>(sacc, scale_log2, m_run, bs);
+    }
+    l_run += lsum;
     if constexpr (STATS) {
 #pragma unroll
-      for (int b = 0; b < TB; ++b) pend[b] = __log2f(bs[b] + __shfl_xor(bs[b], 32)) + mx;
+      for (int b = 0; b < TB; ++b) pend[b] = __log2f(bs[b] + __shfl_xor(bs[b], 32)) + m_run;
     }
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -201,7 +242,7 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     return;
   }
 
-  // padding rows contribute exp2(x - inf) = 0 to every mass
+  // padding rows (Q = 0, finite scores) contribute exp2(-inf) = 0 to every mass
   const float sub = qvalid ? lse2 : INFINITY;
 
   // ---- sweep 2: block masses -----------------------------------------------
@@ -215,17 +256,9 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     f32x16_t sacc[C::KB];
     tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
+    if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
     float acc[TB];
-#pragma unroll
-    for (int b = 0; b < TB; ++b) acc[b] = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        const int key = kb * 32 + ((t >> 2) << 3) + (g << 2) + (t & 3);
-        const float x = key < kvalid ? sacc[kb][t] * scale_log2 : -INFINITY;
-        acc[kb / SPB] += fast_exp2(x - sub);
-      }
+    tile_sums<C::KB, TB>(sacc, scale_log2, sub, acc);
 #pragma unroll
     for (int b = 0; b < TB; ++b) {
       const float a = wave_sum(acc[b]);
