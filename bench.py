@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clock-context", action="store_true",
+                    help="skip the shader-clock samples and the bf16 GEMM reference")
     ap.add_argument("--no-dense-compare", action="store_true",
                     help="skip the untimed dense-attention comparison, which runs the sparse "
                          "kernel over a full support (for profiles of the sparse launches alone)")
@@ -179,6 +181,85 @@ def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
             "kind": "oracle",
             "sample": f"fp64 oracle Eq.(4) on {n} of {rows} CSR rows (random, seed 0) of one "
                       f"reuse step, {dt:.1f} s, scaled by rows; host {os.cpu_count()} cpus"}
+
+
+def _sclk_sampler():
+    """Background sampler of the GPU shader clock (rocm-smi --showclocks), in MHz."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    exe = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi"
+                                       if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
+    state = {"phase": None, "stop": False, "samples": []}
+
+    def loop():
+        while not state["stop"]:
+            try:
+                out = subprocess.run([exe, "--showclocks"], capture_output=True, text=True,
+                                     timeout=5).stdout
+                m = re.search(r"sclk clock level:\s*\d+:\s*\((\d+)\s*Mhz\)", out, re.I)
+                if m and state["phase"]:
+                    state["samples"].append((state["phase"], int(m.group(1))))
+            except Exception:  # noqa: BLE001 - a missing or failing tool only loses samples
+                pass
+            time.sleep(0.2)
+
+    th = None
+    if exe:
+        th = threading.Thread(target=loop, daemon=True)
+        th.start()
+    return state, th
+
+
+def clock_context(torch, run_fwd, fwd_flop):
+    """Shader clock while the sparse forward runs back to back, and a hipBLASLt
+    bf16 GEMM (8192^3) with its clock, for context on the MFMA fraction: under
+    sustained load the chip runs below the 2.4 GHz behind the 2.5 PFLOP/s peak."""
+    state, th = _sclk_sampler()
+    if th is None:
+        return None
+
+    def loop(fn, flop, secs, phase):
+        fn()
+        torch.cuda.synchronize()
+        state["phase"] = phase
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n, t0 = 0, time.perf_counter()
+        a.record()
+        while time.perf_counter() - t0 < secs:
+            for _ in range(4):
+                fn()
+            n += 4
+            torch.cuda.synchronize()
+        b.record()
+        torch.cuda.synchronize()
+        state["phase"] = None
+        return flop / (a.elapsed_time(b) / n * 1e-3) / 1e12
+
+    fwd_tf = loop(run_fwd, fwd_flop, 2.5, "fwd")
+    x = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    y = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    gemm_tf = loop(lambda: torch.mm(x, y), 2.0 * 8192 ** 3, 2.5, "gemm")
+    del x, y
+    state["stop"] = True
+    th.join(timeout=10)
+
+    def med(phase):
+        v = sorted(c for p, c in state["samples"] if p == phase)
+        return v[len(v) // 2] if v else None
+
+    f_fwd, f_gemm = med("fwd"), med("gemm")
+    out = {"sclk_mhz_sparse_fwd": f_fwd, "sparse_fwd_tflops_back_to_back": round(fwd_tf, 1),
+           "gemm_bf16_8192_tflops": round(gemm_tf, 1), "sclk_mhz_gemm": f_gemm,
+           "samples": len(state["samples"])}
+    if f_fwd:
+        out["sparse_fwd_frac_of_peak_at_its_sclk"] = round(
+            fwd_tf / (MFMA_BF16_PEAK_TFLOPS * f_fwd / 2400.0), 4)
+    if f_gemm:
+        out["gemm_frac_of_peak_at_its_sclk"] = round(
+            gemm_tf / (MFMA_BF16_PEAK_TFLOPS * f_gemm / 2400.0), 4)
+    return out
 
 
 def main():
@@ -390,6 +471,11 @@ def main():
         "hbm": hbm,
         "recall": recall,
     }
+    if not args.no_clock_context and w.dtype == "bf16":
+        q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)
+        res["clock_context"] = clock_context(
+            torch, lambda: L.losa_sparse_attn_fwd(q, k, v, N, C, Ck, row_ptr, col_idx, out=out,
+                                                  workspace=ws_fwd), retained_flop)
     if not args.no_cpu_baseline:
         q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)
         res["cpu_baseline"] = cpu_baseline(w, q, k, v, row_ptr, col_idx, args.cpu_seconds)

@@ -74,4 +74,53 @@ __device__ __forceinline__ int xcd_remap(int id, int total) {
   return (id & 7) * per + (id >> 3);
 }
 
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base + bytes) in scalar registers (the
+// fields make_rsrc fills): an offset outside the range reads zero.
+__device__ __forceinline__ i32x4_t rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// One wave-wide 16-byte-per-lane buffer load straight into LDS: lane L's 16
+// bytes at rs + voff + soff land at LDS byte lds + 16 L (lds wave-uniform).
+// Written as inline assembly so that the compiler does not hold the LDS reads
+// that follow it until it completes: the kernel guarantees they never touch
+// the slot it writes, and waits for it explicitly (vmcnt) before the barrier
+// that publishes the slot.  M0 carries the LDS address; the compiler emits
+// no M0 use of its own in these kernels, so nothing it keeps there is lost.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // M0 is reserved: see above
+__device__ __forceinline__ void dma16(uint32_t lds, const i32x4_t& rs, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rs), "s"(soff) : "m0");
+}
+#pragma clang diagnostic pop
+
+// max / sum of a value and the one held by lane ^ 32 (v_permlane32_swap gives
+// each lane the pair {own, partner} in some order; max and + do not care).
+__device__ __forceinline__ float max_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
+
+// 16-byte LDS read at byte address `addr` (+ a compile-time immediate).
+__device__ __forceinline__ bf16x8_t lds_read16(uint32_t addr) {
+  return *reinterpret_cast<lds_bf16x8_t*>(addr);
+}
+
 }  // namespace losa
