@@ -467,9 +467,13 @@ __global__ void __launch_bounds__(BLK * 2)
       // padding sub-tile past the real stream is masked whole
       const int kvb = (R * u + H < S_real) ? N - jc[H / NS] * BK : 0;
       if (kvb < (H % NS + 1) * 32) mask_sub(cur, H % NS, kvb, g);
+      // raised wave priority while the matrix cores are fed: when both waves
+      // of a SIMD have instructions ready, the one inside its MFMA stream issues
+      __builtin_amdgcn_s_setprio(1);
       float ls = pipeline_step<D, BLK, BK, 4, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
                                           ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc,
                                           cur, scale_log2, m_run, pb[H & 1], issue);
+      __builtin_amdgcn_s_setprio(0);
       // The probabilities of s were taken against the running max without
       // looking at this sub-tile's scores.  If a lane's sum exceeds the bound
       // (or is inf: the first sub-tile, or a jump of the max), raise the max
