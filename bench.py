@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache forward timings (512 MiB write before each call)")
     ap.add_argument("--no-clock-context", action="store_true",
                     help="skip the shader-clock samples and the bf16 GEMM reference")
     ap.add_argument("--no-dense-compare", action="store_true",
@@ -150,37 +152,71 @@ def record_traffic(fetch_csv: str, write_csv: str, copy_mib: int, workload: str)
     print(json.dumps(res))
 
 
-def cpu_baseline(w, q, k, v, rp, ci, budget_s: float):
-    """Time the fp64 oracle's Eq. (4) on a sample of CSR rows; scale to a layer."""
-    import numpy as np
-
-    from oracle import losa_oracle as O
+def _host_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
+    except Exception:  # noqa: BLE001 - threadpoolctl missing: report the cpu count
         threads = os.cpu_count() or 1
+    return {"nproc": os.cpu_count(), "cpu_model": model, "blas_threads": int(threads)}
+
+
+def cpu_baseline(w, q, k, v, mass, rp, ci, budget_s: float):
+    """Time the fp64 oracle on the host cores, per layer, for its three phases:
+    calibration (Eq. (1)) and the sparse forward (Eq. (4)) on samples of query
+    blocks / CSR rows scaled by the row count, selection (Eq. (3)) on every row.
+    `value` is the sparse forward, the counterpart of the metric."""
+    import numpy as np
+
+    from oracle import losa_oracle as O
+    host = _host_info()
     f64 = lambda x: x.float().cpu().numpy().astype(np.float64)  # noqa: E731
     qh, kh, vh = f64(q), f64(k), f64(v)
     rp_h = rp.cpu().numpy().astype(np.int64)
     ci_h = ci[:rp_h[-1]].cpu().numpy().astype(np.int64)
     rows = rp_h.size - 1
     order = np.random.default_rng(0).permutation(rows)
-    # rows in chunks, in a fixed random order, until the time budget is spent
-    n, dt, chunk = 0, 0.0, 8
-    while n < rows and dt < budget_s:
-        part = order[n:n + chunk]
-        t0 = time.perf_counter()
-        O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h,
-                           rows_subset=part)
-        dt += time.perf_counter() - t0
-        n += part.size
-        chunk = min(2 * chunk, 64)
-    ms_layer = dt / n * rows * 1e3
-    return {"value": round(ms_layer, 1), "unit": "ms/layer", "cores": int(threads),
+
+    def sampled(fn, budget):
+        # rows in chunks, in a fixed random order, until the time budget is spent
+        n, dt, chunk = 0, 0.0, 4
+        while n < rows and dt < budget:
+            part = order[n:n + chunk]
+            t0 = time.perf_counter()
+            fn(part)
+            dt += time.perf_counter() - t0
+            n += part.size
+            chunk = min(2 * chunk, 64)
+        return dt / n * rows * 1e3, n, dt
+
+    fwd_ms, n_f, dt_f = sampled(lambda part: O.sparse_attention(
+        qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_h, ci_h, rows_subset=part), budget_s * 2 / 3)
+    cal_ms, n_c, dt_c = sampled(lambda part: O.block_masses(
+        qh, kh, w.N, w.block, w.bk, w.scale, rows_subset=part), budget_s / 3)
+    mh = f64(mass)
+    t0 = time.perf_counter()
+    O.select_blocks(mh, w.N, w.block, w.bk, w.tau)
+    sel_ms = (time.perf_counter() - t0) * 1e3
+    return {"value": round(fwd_ms, 1), "unit": "ms/layer", "cores": host["blas_threads"],
             "kind": "oracle",
-            "sample": f"fp64 oracle Eq.(4) on {n} of {rows} CSR rows (random, seed 0) of one "
-                      f"reuse step, {dt:.1f} s, scaled by rows; host {os.cpu_count()} cpus"}
+            "sample": f"fp64 oracle Eq.(4) on {n_f} of {rows} CSR rows (random, seed 0) of one "
+                      f"reuse step, {dt_f:.1f} s, scaled by rows",
+            "phases_ms_per_layer": {
+                "calibrate": round(cal_ms, 1), "select": round(sel_ms, 1),
+                "sparse_fwd": round(fwd_ms, 1)},
+            "phase_samples": {"calibrate": f"Eq.(1) on {n_c} of {rows} query blocks, "
+                                           f"{dt_c:.1f} s, scaled by rows",
+                              "select": f"Eq.(3) on all {rows} rows"},
+            "host": host}
 
 
 def _sclk_sampler():
@@ -392,6 +428,26 @@ def main():
                                                        out=out, workspace=ws_fwd))
         del rp_full, ci_full
 
+    # ---- cold forward: a 512 MiB write before each call evicts L2 and the
+    # 256 MB Infinity Cache (the write is outside the events) -------------------
+    cold = None
+    if not args.no_cold:
+        scratch = torch.empty((512 << 20) // 4, dtype=torch.float32, device=dev)
+        evs = []
+        for t in range(8):
+            q, k, v = reuse_inputs[t % len(reuse_inputs)] if reuse_inputs else (q0, k0, v0)
+            scratch.fill_(float(t))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            L.losa_sparse_attn_fwd(q, k, v, N, C, Ck, row_ptr, col_idx, out=out,
+                                   workspace=ws_fwd)
+            b.record()
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        ct = sorted(a.elapsed_time(b) for a, b in evs)
+        cold = {"median": round(ct[len(ct) // 2], 4), "min": round(ct[0], 4), "calls": len(ct)}
+        del scratch
+
     # ---- recall of the frozen support at later steps (Eq. (2)) --------------
     recall = {}
     for t in sorted({1, (reuse + 1) // 2, reuse}):
@@ -450,12 +506,14 @@ def main():
         },
         "fwd_ms": {"mean": round(fwd, 4), "median": round(fwd_sorted[len(fwd_sorted) // 2], 4),
                    "min": round(fwd_sorted[0], 4)},
+        "fwd_cold_ms": cold,
         "construct_ms": round(con_t, 3),
         "select_ms": round(sel_t, 3),
         "calibrate_alone_ms": round(cal_t, 3),
         "calibrate_two_sweep_ms": round(cal2_t, 3),
         "dense_attn_ms": round(dense_t, 3) if dense_t else None,
         "construct_over_dense": round(con_t / dense_t, 3) if dense_t else None,
+        "kernel_speedup_vs_full_csr": round(dense_t / fwd, 3) if dense_t else None,
         "retained_tflops": round(achieved, 1),
         "dense_equiv_tflops": round(dense_flop / (fwd * 1e-3) / 1e12, 1),
         "kernel_speedup_vs_dense_flops": round(dense_flop / retained_flop, 3),
@@ -478,7 +536,7 @@ def main():
                                                   workspace=ws_fwd), retained_flop)
     if not args.no_cpu_baseline:
         q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)
-        res["cpu_baseline"] = cpu_baseline(w, q, k, v, row_ptr, col_idx, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, q, k, v, mass, row_ptr, col_idx, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 
