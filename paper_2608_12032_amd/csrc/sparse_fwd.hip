@@ -28,8 +28,9 @@
 // therefore stores, within every group of 16 keys, positions 4..7 and 8..11
 // swapped (an involution), so each lane's 8 keys are 16 contiguous bytes.
 //
-// Streaming.  The row's keys are a stream of 32-key sub-tiles (NS = BLK/32 per
-// key block).  K and V^T sub-tiles pass through two rings of kRing LDS slots,
+// Streaming.  The row's keys are a stream of 32-key sub-tiles (NS = BK/32 per
+// key block of BK keys; with BK = 32 the stream is padded to whole loop passes
+// with sub-tiles whose keys are all masked).  K and V^T sub-tiles pass through two rings of kRing LDS slots,
 // filled by 16-byte buffer loads that write LDS directly.  Sub-iteration s
 // reads K sub-tile s+1 (scores of the next sub-tile) and V^T sub-tile s-1
 // (P V of the previous one); after the barrier that opens it, the slots that
@@ -48,6 +49,21 @@
 // LDS image of its sub-tiles (written by the transpose kernel), so its loads
 // are plain contiguous copies.  Both swizzles make the 16 rows read by one
 // 16-lane group of an operand read land in distinct banks.
+//
+// Softmax.  Probabilities are taken against the running max without looking
+// at the sub-tile's scores first; only when a lane's sub-tile sum exceeds
+// kSumBound (or is inf) is the max raised and the sub-tile redone, so every
+// probability entering P V is at most kSumBound.
+//
+// Dense mode (template flag DENSE; the construction step).  Every row keeps
+// every key block holding a valid key, rows run in id order, and per key block
+// each query's probability sum is stored as a block statistic
+// a(q, j) = log2(sum) + m (the reference m it was taken against), from which
+// the block masses follow once lse is known (stat_mass_kernel).
+//
+// Dispatch order (sparse mode).  Rows run longest first inside chunks of
+// neighbouring query blocks, each XCD on a contiguous range of rows
+// (order_rows_kernel), so rows in flight share their key blocks in L2.
 //
 // Padding.  Keys >= N get score -inf (only the ragged last block needs it).
 // Query rows >= N are written as 0 with lse = -inf; so are rows with an empty
