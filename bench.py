@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the density sweep (Wan shape, tau x locality weight) instead of "
+                         "the default step; prints one JSON line with every point")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold-cache forward timings (512 MiB write before each call)")
     ap.add_argument("--no-clock-context", action="store_true",
@@ -324,8 +327,67 @@ def clock_context(torch, run_fwd, fwd_flop):
     return out
 
 
+def run_sweep(args):
+    """Density sweep at the Wan shape: for each locality weight alpha one set of
+    inputs and one calibration, then per tau the selection and the sparse
+    forward (median of `reps` HIP-event-timed calls after warm-up), its
+    coverage, MFMA fraction and the speedup over the full support (tau = 1)."""
+    import torch
+
+    from paper_2608_12032_amd import losa as L
+    from paper_2608_12032_amd import workload as W
+
+    pts = W.sweep_points()
+    if args.block_k:
+        pts = [W.rectangular(p, args.block_k) for p in pts]
+    reps = max(3, args.steps * 5)
+    out = []
+    for alpha in W.SWEEP_ALPHAS:
+        group = [p for p in pts if p.alpha == alpha]
+        w = group[0]
+        N, C, Ck, d = w.N, w.block, w.bk, w.d
+        q, k, v = W.make_inputs(w, device="cuda")
+        mass, _ = L.losa_calibrate_mass(q, k, N, C, Ck, want_lse=False)
+        o = torch.empty_like(q)
+        ws = torch.empty(L.workspace_bytes(2, 1, w.B, w.H, N, d, C, Ck), dtype=torch.uint8,
+                         device="cuda")
+        times = {}
+        for p in group:
+            rp, ci = L.losa_select_blocks(mass, N, C, Ck, p.tau)
+            nnz = L.nnz(rp)
+            for _ in range(max(1, args.warmup)):
+                L.losa_sparse_attn_fwd(q, k, v, N, C, Ck, rp, ci, out=o, workspace=ws)
+            evs = []
+            for _ in range(reps):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                L.losa_sparse_attn_fwd(q, k, v, N, C, Ck, rp, ci, out=o, workspace=ws)
+                b.record()
+                evs.append((a, b))
+            torch.cuda.synchronize()
+            ms = sorted(a.elapsed_time(b) for a, b in evs)[reps // 2]
+            flop = 4.0 * C * Ck * d * nnz
+            times[p.tau] = ms
+            out.append({"alpha": alpha, "tau": p.tau, "coverage": round(nnz / (rp.numel() - 1)
+                                                                         / w.n_kblocks, 4),
+                        "fwd_ms_median": round(ms, 4),
+                        "mfma_frac": round(flop / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)})
+        for e in out:
+            if e["alpha"] == alpha:
+                e["speedup_vs_tau1"] = round(times[1.0] / e["fwd_ms_median"], 3)
+        del q, k, v, mass, o, ws
+    w0 = pts[0]
+    print(json.dumps({"sweep": f"{w0.name}: Wan shape B={w0.B} H={w0.H} d={w0.d} N={w0.N} "
+                               + (f"block {w0.block}" if w0.bk == w0.block
+                                  else f"blocks {w0.block}x{w0.bk}"),
+                      "unit": "ms/layer", "reps": reps, "points": out}), flush=True)
+
+
 def main():
     args = parse()
+    if args.sweep:
+        run_sweep(args)
+        return
     if args.record_traffic:
         record_traffic(*args.record_traffic, args.copy_reference_mib, args.workload)
         return
