@@ -13,8 +13,10 @@
 //
 // Two sweeps (no workspace): a workgroup (one query block, BLK/32 waves of 32
 // query rows) sweeps the key tiles of its head twice:
-//   1. S^T = K Q^T per tile, running max and running sum -> lse_q (log2
-//      domain) per query, kept in registers;
+//   1. S^T = K Q^T per tile and a running sum of 2^(x - m) -> lse_q (log2
+//      domain) per query, kept in registers.  The reference m is raised only
+//      when a lane's tile sum passes 2^20 (or is inf: the first tile), so a
+//      score costs one fma, one exp2 and one add;
 //   2. S^T again (identical MFMA order, so identical scores), p = exp2(x -
 //      lse2_q), summed per lane, then across the wave; each wave parks its
 //      per-tile partial in LDS and the workgroup adds the waves' partials in a
