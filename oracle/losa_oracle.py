@@ -296,7 +296,7 @@ def sparse_attention(q, k, v, N: int, block_q: int, block_k: int, scale: float,
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     col_idx = np.asarray(col_idx, dtype=np.int64)
     B, H, Np, d = q.shape
-    n_q = Np // block_q
+    n_q, n_k = Np // block_q, Np // block_k
     o = np.zeros((B, H, Np, v.shape[-1]))
     lse = np.full((B, H, Np), -np.inf)
     todo = range(B * H * n_q) if rows_subset is None else rows_subset
@@ -306,7 +306,10 @@ def sparse_attention(q, k, v, N: int, block_q: int, block_k: int, scale: float,
         rows = valid_rows(i, block_q, N)
         if rows.size == 0:
             continue
+        # Omega is a set of key blocks: repeated ids count once, and an id
+        # outside [0, n_k) names no key block (it contributes no key)
         blocks = np.unique(col_idx[row_ptr[r]:row_ptr[r + 1]])
+        blocks = blocks[(blocks >= 0) & (blocks < n_k)]
         keys = (np.concatenate([valid_keys(int(j), block_k, N) for j in blocks])
                 if blocks.size else np.zeros(0, dtype=np.int64))
         if keys.size == 0:

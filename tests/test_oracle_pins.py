@@ -413,6 +413,34 @@ def check_token_mask_equals_blockwise(seed=8, R=8, C=4, tau=0.8) -> bool:
     return bool(rp[-1] < 2 * (Np // R) * (Np // C) and np.allclose(o_b, o_t, rtol=0, atol=1e-12))
 
 
+def check_out_of_range_ids_ignored(seed=9, R=8, C=4) -> bool:
+    """A CSR with unordered, repeated and out-of-range ids (negative and >= n_k)
+    against the token-level mask, which by construction only ever matches
+    key blocks 0 .. n_kv-1."""
+    rng = np.random.default_rng(seed)
+    N, Np, d = 37, 40, 8
+    q, k, v = _rand_qkv(rng, N=N, Np=Np, d=d, scale_qk=1.4)
+    scale = 1 / math.sqrt(d)
+    rows = q.shape[0] * q.shape[1] * (Np // R)
+    n_k = Np // C
+    lens = rng.integers(0, n_k + 4, size=rows)
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    ci = rng.integers(-3, n_k + 3, size=int(rp[-1])).astype(np.int64)
+    if not ((ci < 0).any() and (ci >= n_k).any()):
+        return False
+    o_b, _ = O.sparse_attention(q, k, v, N, R, C, scale, rp, ci)
+    o_t = O.token_mask_attention(q, k, v, N, R, C, scale, rp, ci)
+    # and with the out-of-range ids removed beforehand
+    keep = (ci >= 0) & (ci < n_k)
+    rp2 = np.concatenate([[0], np.cumsum([keep[rp[i]:rp[i + 1]].sum() for i in range(rows)])])
+    o_c, _ = O.sparse_attention(q, k, v, N, R, C, scale, rp2.astype(np.int64), ci[keep])
+    return bool(np.allclose(o_b, o_t, rtol=0, atol=1e-12) and np.array_equal(o_b, o_c))
+
+
+def test_out_of_range_ids_are_ignored():
+    assert check_out_of_range_ids_ignored()
+
+
 @pytest.mark.parametrize("R,C", [(8, 8), (8, 4), (4, 8)])
 def test_token_mask_brute_force(R, C):
     assert check_token_mask_equals_blockwise(R=R, C=C)
@@ -527,6 +555,13 @@ def _sparse_no_scale(q, k, v, N, R, C, scale, rp, ci, rows_subset=None):
     return _orig_sparse(q, k, v, N, R, C, 1.0, rp, ci, rows_subset)
 
 
+def _sparse_ids_wrap(q, k, v, N, R, C, scale, rp, ci, rows_subset=None):
+    # a negative block id taken modulo n_k instead of being ignored
+    ci = np.asarray(ci, dtype=np.int64)
+    n_k = np.asarray(q).shape[2] // C
+    return _orig_sparse(q, k, v, N, R, C, scale, rp, np.where(ci < 0, ci % n_k, ci), rows_subset)
+
+
 def _masses_sum_not_mean(q, k, N, R, C, scale):
     mbar, lse = _orig_masses(q, k, N, R, C, scale)
     return mbar * R, lse
@@ -565,7 +600,7 @@ _orig_topk = O.select_row_topk
 ALL_PINS = [check_golden, check_dense_vs_sdpa, check_sparse_full_equals_dense,
             check_masses_brute_force, check_selection_brute_force,
             check_token_mask_equals_blockwise, check_topk_brute_force,
-            check_recall_closed_form]
+            check_recall_closed_form, check_out_of_range_ids_ignored]
 
 
 def _some_pin_fails():
@@ -586,6 +621,7 @@ def _some_pin_fails():
     ("select_row", _select_row_strict),
     ("sparse_attention", _sparse_v_is_k),
     ("sparse_attention", _sparse_no_scale),
+    ("sparse_attention", _sparse_ids_wrap),
     ("block_masses", _masses_sum_not_mean),
     ("block_masses", _masses_include_padding),
     ("select_row_topk", _topk_off_by_one),
