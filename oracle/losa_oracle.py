@@ -168,9 +168,16 @@ def mass_order(mrow: np.ndarray) -> np.ndarray:
     return np.lexsort((idx, -np.asarray(mrow, dtype=np.float64)))
 
 
+def clean_masses(mrow) -> np.ndarray:
+    """Masses as the selection reads them: a mass is a probability sum, so a
+    negative or NaN entry (a corrupt input) counts as 0."""
+    m = np.asarray(mrow, dtype=np.float64)
+    return np.where(m > 0, m, 0.0)
+
+
 def select_row(mrow, tau: float, n_k_valid: int, has_valid_rows: bool = True) -> RowSelection:
     """Eq. (3): the shortest prefix of the mass order whose sum reaches tau."""
-    mrow = np.asarray(mrow, dtype=np.float64)
+    mrow = clean_masses(mrow)
     order = mass_order(mrow)
     cum = np.cumsum(mrow[order])
     if not has_valid_rows:
@@ -222,7 +229,7 @@ def select_row_topk(mrow, k: int, n_k_valid: int, has_valid_rows: bool = True) -
     the row in the same order as Eq. (3)'s (ties: smaller index first), k
     clamped to the blocks that hold a valid key.  Padding-only blocks carry no
     mass and have the largest indices, so they never enter while k <= n_k_valid."""
-    mrow = np.asarray(mrow, dtype=np.float64)
+    mrow = clean_masses(mrow)
     order = mass_order(mrow)
     cum = np.cumsum(mrow[order])
     s = min(int(k), n_k_valid) if has_valid_rows else 0

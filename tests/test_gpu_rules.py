@@ -253,3 +253,28 @@ def test_construct_full_size_wan_sampled(L):
         lo, hi = i * w.block, min((i + 1) * w.block, w.N)
         err = np.abs(og[0, h, lo:hi] - o_ref[0, h, lo:hi])
         assert err.max() <= 2e-2 and err.mean() <= 2e-3
+
+
+def test_corrupt_masses_select_like_zeros(L):
+    """Negative and NaN masses count as 0 in both selection rules (reading of
+    the selection for corrupt inputs): the GPU's sets equal the oracle's."""
+    w = CASES["wan-small"]
+    q, k, _ = W.make_inputs(w, device="cuda")
+    mass, _ = L.losa_calibrate_mass(q, k, w.N, w.block, w.bk, want_lse=False)
+    torch.cuda.synchronize()
+    m = f64(mass)
+    rng = np.random.default_rng(12)
+    bad = rng.random(m.shape) < 0.2
+    m[bad] = np.where(rng.random(bad.sum()) < 0.5, np.nan, -rng.random(bad.sum()))
+    mt = torch.tensor(m, dtype=torch.float32, device="cuda")
+    m32 = m.astype(np.float32).astype(np.float64)
+    for tau in (0.5, 0.9, 0.99):
+        rp, ci = L.losa_select_blocks(mt, w.N, w.block, w.bk, tau)
+        rp_o, ci_o, _ = O.select_blocks(m32, w.N, w.block, w.bk, float(np.float32(tau)))
+        rp_g, ci_g = host_csr(rp, ci)
+        assert np.array_equal(rp_g, rp_o) and np.array_equal(ci_g, ci_o), tau
+    for kk in (1, 7, 30):
+        rp, ci = L.losa_select_blocks_topk(mt, w.N, w.block, w.bk, kk)
+        rp_o, ci_o, _ = O.select_blocks_topk(m32, w.N, w.block, w.bk, kk)
+        rp_g, ci_g = host_csr(rp, ci)
+        assert np.array_equal(rp_g, rp_o) and np.array_equal(ci_g, ci_o), kk

@@ -261,6 +261,34 @@ def test_selection_nested_and_recall_at_least_tau():
     assert covs == sorted(covs) and covs[-1] == 1.0
 
 
+def check_corrupt_masses_count_as_zero(seed=11) -> bool:
+    """Negative and NaN masses select exactly like zeros (both rules); the pin
+    is the same row with those entries written as 0 by hand."""
+    rng = np.random.default_rng(seed)
+    ok = True
+    for _ in range(20):
+        n = int(rng.integers(3, 12))
+        m = rng.dirichlet(np.ones(n))
+        bad = rng.random(n) < 0.3
+        if not bad.any():
+            bad[0] = True
+        corrupt = m.copy()
+        corrupt[bad] = np.where(rng.random(bad.sum()) < 0.5, np.nan, -rng.random(bad.sum()))
+        clean = m.copy()
+        clean[bad] = 0.0
+        for tau in (0.5, 0.9, 0.999):
+            a, b = O.select_row(corrupt, tau, n), O.select_row(clean, tau, n)
+            ok &= np.array_equal(a.omega, b.omega) and a.s == b.s
+        for kk in (1, n // 2, n):
+            a, b = O.select_row_topk(corrupt, kk, n), O.select_row_topk(clean, kk, n)
+            ok &= np.array_equal(a.omega, b.omega)
+    return bool(ok)
+
+
+def test_corrupt_masses_count_as_zero():
+    assert check_corrupt_masses_count_as_zero()
+
+
 def test_padding_only_blocks_are_never_kept():
     # block_k smaller than the padding tail: key blocks made only of padding
     rng = np.random.default_rng(7)
@@ -562,6 +590,11 @@ def _sparse_ids_wrap(q, k, v, N, R, C, scale, rp, ci, rows_subset=None):
     return _orig_sparse(q, k, v, N, R, C, scale, rp, np.where(ci < 0, ci % n_k, ci), rows_subset)
 
 
+def _clean_masses_kept_negative(mrow):
+    # corrupt masses read as they are instead of as 0
+    return np.asarray(mrow, dtype=np.float64)
+
+
 def _masses_sum_not_mean(q, k, N, R, C, scale):
     mbar, lse = _orig_masses(q, k, N, R, C, scale)
     return mbar * R, lse
@@ -600,7 +633,8 @@ _orig_topk = O.select_row_topk
 ALL_PINS = [check_golden, check_dense_vs_sdpa, check_sparse_full_equals_dense,
             check_masses_brute_force, check_selection_brute_force,
             check_token_mask_equals_blockwise, check_topk_brute_force,
-            check_recall_closed_form, check_out_of_range_ids_ignored]
+            check_recall_closed_form, check_out_of_range_ids_ignored,
+            check_corrupt_masses_count_as_zero]
 
 
 def _some_pin_fails():
@@ -622,6 +656,7 @@ def _some_pin_fails():
     ("sparse_attention", _sparse_v_is_k),
     ("sparse_attention", _sparse_no_scale),
     ("sparse_attention", _sparse_ids_wrap),
+    ("clean_masses", _clean_masses_kept_negative),
     ("block_masses", _masses_sum_not_mean),
     ("block_masses", _masses_include_padding),
     ("select_row_topk", _topk_off_by_one),
