@@ -22,7 +22,7 @@ from oracle import losa_oracle as O
 pytestmark = pytest.mark.gpu
 
 BLOCKS = [(64, 64), (128, 128), (128, 32), (64, 32)]
-SEEDS = list(range(24))
+SEEDS = list(range(48))
 
 
 @pytest.fixture(scope="module")
@@ -42,7 +42,7 @@ def draw(seed):
     return dict(B=int(rng.integers(1, 3)), H=int(rng.integers(1, 4)),
                 N=int(rng.integers(1, 700)), d=int(rng.choice([64, 128])), Cq=Cq, Ck=Ck,
                 dtype=str(rng.choice(["bf16", "f32"])),
-                tau=float(rng.choice([0.5, 0.9, 0.99, 0.999, 1.0])),
+                tau=float(rng.choice([0.1, 0.5, 0.9, 0.99, 0.999, 1.0])),
                 spread=float(rng.uniform(0.5, 3.0)), rng=rng)
 
 
