@@ -420,16 +420,25 @@ def test_padding_contents_are_ignored(L, key):
         assert cmp["ok"], cmp
 
 
-def test_deterministic(L):
-    w = SMALL["cog-bf16-d64-ragged"]
+@pytest.mark.parametrize("key", ["cog-bf16-d64-ragged", "wan-bf16-d128-r128c32"])
+def test_deterministic(L, key):
+    """Every entry point twice on the same inputs: bitwise equal results (no
+    atomics, fixed reduction orders)."""
+    w = SMALL[key]
+    N, Cq, Ck = w.N, w.block, w.bk
     q, k, v = W.make_inputs(w, device="cuda")
     outs = []
     for _ in range(2):
-        mass, lse = L.losa_calibrate_mass(q, k, w.N, w.block)
-        rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.block, w.tau)
-        o = L.losa_sparse_attn_fwd(q, k, v, w.N, w.block, w.block, rp, ci)
+        mass, lse = L.losa_calibrate_mass(q, k, N, Cq, Ck)
+        mass2, lse2 = L.losa_calibrate_mass(q, k, N, Cq, Ck, two_sweep=True)
+        rp, ci = L.losa_select_blocks(mass, N, Cq, Ck, w.tau)
+        rk, ck = L.losa_select_blocks_topk(mass, N, Cq, Ck, 5)
+        o, lo = L.losa_sparse_attn_fwd(q, k, v, N, Cq, Ck, rp, ci, want_lse=True)
+        rr, rh = L.losa_block_recall(mass2, N, Cq, Ck, rp, ci)
+        oc, mc, lc = L.losa_construct(q, k, v, N, Cq, Ck, want_lse=True)
         torch.cuda.synchronize()
-        outs.append((mass.clone(), lse.clone(), rp.clone(), ci[:L.nnz(rp)].clone(), o.clone()))
+        outs.append([t.clone() for t in (mass, lse, mass2, lse2, rp, ci[:L.nnz(rp)], rk,
+                                         ck[:L.nnz(rk)], o, lo, rr, rh, oc, mc, lc)])
     for a, b in zip(*outs):
         assert torch.equal(a, b)
 
