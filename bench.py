@@ -248,6 +248,30 @@ def cpu_baseline(w, q, k, v, mass, rp, ci, budget_s: float):
             "host": host}
 
 
+def tiny_single_thread():
+    """The oracle's three phases on the Tiny configuration (B=1, H=2, d=64, fp32,
+    N=1,024, block 64, tau=0.99), whole, on one host thread: a second CPU figure
+    that needs no sampling or scaling."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import losa_oracle as O
+    from paper_2608_12032_amd import workload as W
+    tw = W.WORKLOADS["tiny"]
+    q, k, v = (x.cpu().numpy().astype(np.float64) for x in W.make_inputs(tw))
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        mbar, _ = O.block_masses(q, k, tw.N, tw.block, tw.bk, tw.scale)
+        t1 = time.perf_counter()
+        rp, ci, _ = O.select_blocks(mbar, tw.N, tw.block, tw.bk, tw.tau)
+        t2 = time.perf_counter()
+        O.sparse_attention(q, k, v, tw.N, tw.block, tw.bk, tw.scale, rp, ci)
+        t3 = time.perf_counter()
+    return {"threads": 1, "workload": "tiny: B=1 H=2 d=64 f32 N=1024 block 64 tau=0.99",
+            "ms": {"calibrate": round((t1 - t0) * 1e3, 2), "select": round((t2 - t1) * 1e3, 2),
+                   "sparse_fwd": round((t3 - t2) * 1e3, 2)}}
+
+
 def _sclk_sampler():
     """Background sampler of the GPU shader clock (rocm-smi --showclocks), in MHz."""
     import re
@@ -636,6 +660,7 @@ def main():
     if not args.no_cpu_baseline:
         q, k, v = reuse_inputs[-1] if reuse_inputs else (q0, k0, v0)
         res["cpu_baseline"] = cpu_baseline(w, q, k, v, mass, row_ptr, col_idx, args.cpu_seconds)
+        res["cpu_baseline"]["tiny_single_thread"] = tiny_single_thread()
     print(json.dumps(res), flush=True)
 
 

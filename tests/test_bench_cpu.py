@@ -105,3 +105,9 @@ def test_cpu_baseline_reports_three_phases():
     assert set(ph) == {"calibrate", "select", "sparse_fwd"} and min(ph.values()) > 0
     assert r["value"] == ph["sparse_fwd"]
     assert r["host"]["nproc"] >= 1 and r["cores"] >= 1
+
+
+def test_tiny_single_thread_times_the_whole_oracle():
+    r = bench.tiny_single_thread()
+    assert r["threads"] == 1 and r["workload"].startswith("tiny")
+    assert set(r["ms"]) == {"calibrate", "select", "sparse_fwd"} and min(r["ms"].values()) > 0
