@@ -10,6 +10,11 @@
 // and so do rows whose key set is empty; col_idx entries outside [0, n_k) are
 // ignored, a repeated entry counts once (the row's ids are flagged in LDS and
 // walked in ascending order), and row bounds are clamped to [0, col_idx_len].
+//
+// Row sums.  The softmax normaliser is summed per 32-key chunk in fp32 and the
+// chunk sums are carried in an fp64 running sum.  Added one by one to an fp32
+// accumulator, the many small terms of far keys fall below half its ulp and
+// are lost: over 131k keys that biases the sum low by ~2e-4.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -52,7 +57,8 @@ __global__ void __launch_bounds__(BLK)
     q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
     o[dd] = 0.f;
   }
-  float m = kNegBig, l = 0.f;
+  float m = kNegBig;
+  double l = 0.0;
 
   // dense: every key block that holds a valid key (the construction step)
   __shared__ uint8_t flag[kSparseFwdMaxNk];
@@ -89,23 +95,26 @@ __global__ void __launch_bounds__(BLK)
       }
       const float alpha = fast_exp2(m - mx);
       m = mx;
-      l *= alpha;
+      l *= (double)alpha;
 #pragma unroll
       for (int dd = 0; dd < D; ++dd) o[dd] *= alpha;
+      float part = 0.f;
 #pragma unroll
       for (int kk = 0; kk < CK; ++kk) {
         const float p = fast_exp2(s[kk] - m);
-        l += p;
+        part += p;
 #pragma unroll
         for (int dd = 0; dd < D; ++dd) o[dd] = fmaf(p, Vc[kk * D + dd], o[dd]);
       }
+      l += (double)part;
     }
   }
-  const bool ok = (qrow < N) && (l > 0.f);
-  const float inv = ok ? 1.0f / l : 0.f;
+  const float lf = (float)l;
+  const bool ok = (qrow < N) && (lf > 0.f);
+  const float inv = ok ? 1.0f / lf : 0.f;
 #pragma unroll
   for (int dd = 0; dd < D; ++dd) O[head + (size_t)qrow * D + dd] = o[dd] * inv;
-  if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = ok ? (m + __log2f(l)) * kLn2 : -INFINITY;
+  if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = ok ? (m + __log2f(lf)) * kLn2 : -INFINITY;
 }
 
 template <int D, int BLK, int BK>
@@ -135,7 +144,8 @@ __global__ void __launch_bounds__(BLK)
   const int n_kv = (N + BK - 1) / BK;  // key blocks holding a real key
 
   // sweep 1: running max / sum over every valid key
-  float m = kNegBig, l = 0.f;
+  float m = kNegBig;
+  double l = 0.0;
   for (int j = 0; j < n_kv; ++j) {
     const int kvalid = min(BK, N - j * BK);
     for (int c0 = 0; c0 < kvalid; c0 += CK) {
@@ -153,14 +163,16 @@ __global__ void __launch_bounds__(BLK)
         s[kk] = kk < nk ? acc : -INFINITY;
         mx = fmaxf(mx, s[kk]);
       }
-      l *= fast_exp2(m - mx);
+      l *= (double)fast_exp2(m - mx);
       m = mx;
+      float part = 0.f;
 #pragma unroll
-      for (int kk = 0; kk < CK; ++kk) l += fast_exp2(s[kk] - m);
+      for (int kk = 0; kk < CK; ++kk) part += fast_exp2(s[kk] - m);
+      l += (double)part;
     }
   }
   const bool qvalid = qrow < N;
-  const float lse2 = m + __log2f(l);
+  const float lse2 = m + __log2f((float)l);
   if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = qvalid ? lse2 * kLn2 : -INFINITY;
   const float sub = qvalid ? lse2 : INFINITY;
 

@@ -462,6 +462,18 @@ def test_full_size_sampled(L, key):
     say(f"full-{key}: coverage {info['coverage']:.3f} nnz {info['nnz']}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_max_key_blocks(L, dtype):
+    """The largest supported key-block count per head, 4,096 (128 x 32 blocks,
+    N = 130,975 padded to 131,072, ragged last block): every entry point of the
+    pipeline at the limit, sampled rows against the oracle."""
+    w = W.rectangular(W.Workload(f"maxnk-{dtype}", 1, 1, 64, dtype, (31, 65, 65), 128, 0.99,
+                                 1.5, 0.5, 0.02, 0, 83))
+    assert w.n_kblocks == 4096 and w.N < w.N_pad
+    info = run_case(L, w, w.tau, rows=sample_rows(w), label=f"maxnk-{dtype}")
+    say(f"maxnk-{dtype}: coverage {info['coverage']:.3f} nnz {info['nnz']}")
+
+
 @pytest.mark.parametrize("alpha", W.SWEEP_ALPHAS)
 def test_density_sweep_sampled(L, alpha):
     pts = [p for p in W.sweep_points() if p.alpha == alpha]
