@@ -43,6 +43,11 @@ def test_source_hash_ignores_comment_edits_only(tmp_path, monkeypatch):
     assert bench.source_hash() == h0
     f.write_text(text.replace("kSumBound = 1048576.0f", "kSumBound = 524288.0f"))
     assert bench.source_hash() != h0
+    f.write_text(text)
+    # the fp32 path is not among the recorded kernels
+    g = src / "f32_path.hip"
+    g.write_text(g.read_text().replace("constexpr int CK = 32;", "constexpr int CK = 16;"))
+    assert bench.source_hash() == h0
 
 
 def _counter_csv(path, counter, rows):
