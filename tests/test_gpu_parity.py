@@ -470,8 +470,29 @@ def test_max_key_blocks(L, dtype):
     w = W.rectangular(W.Workload(f"maxnk-{dtype}", 1, 1, 64, dtype, (31, 65, 65), 128, 0.99,
                                  1.5, 0.5, 0.02, 0, 83))
     assert w.n_kblocks == 4096 and w.N < w.N_pad
-    info = run_case(L, w, w.tau, rows=sample_rows(w), label=f"maxnk-{dtype}")
+    rows = sample_rows(w)
+    info = run_case(L, w, w.tau, rows=rows, label=f"maxnk-{dtype}")
     say(f"maxnk-{dtype}: coverage {info['coverage']:.3f} nnz {info['nnz']}")
+    # the construction step at the limit: masses, and the dense output through
+    # the oracle's Eq. (4) over every valid key block (dense attention)
+    q, k, v = W.make_inputs(w, device="cuda")
+    o, mass = L.losa_construct(q, k, v, w.N, w.block, w.bk)
+    torch.cuda.synchronize()
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    n_q, n_k = w.n_blocks, w.n_kblocks
+    n_kv = O.num_valid_key_blocks(w.N, w.bk)
+    m_ref, _ = O.block_masses(qh, kh, w.N, w.block, w.bk, w.scale, rows_subset=rows)
+    rp_full = np.arange(0, (n_q + 1) * n_kv, n_kv)
+    ci_full = np.tile(np.arange(n_kv), n_q)
+    o_ref, _ = O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_full, ci_full,
+                                  rows_subset=rows)
+    mg, og = f64(mass).reshape(-1, n_k), f64(o)
+    tmax, tmean = out_tol(w)
+    for r in rows:
+        assert np.abs(mg[r] - m_ref.reshape(-1, n_k)[r]).max() <= MASS_TOL
+        lo, hi = r * w.block, min((r + 1) * w.block, w.N)
+        err = np.abs(og[0, 0, lo:hi] - o_ref[0, 0, lo:hi])
+        assert err.max() <= tmax and err.mean() <= tmean
 
 
 @pytest.mark.parametrize("alpha", W.SWEEP_ALPHAS)
