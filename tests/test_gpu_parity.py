@@ -493,6 +493,21 @@ def test_max_key_blocks(L, dtype):
         lo, hi = r * w.block, min((r + 1) * w.block, w.N)
         err = np.abs(og[0, 0, lo:hi] - o_ref[0, 0, lo:hi])
         assert err.max() <= tmax and err.mean() <= tmean
+    # recall of the threshold support and the top-k rule at the limit, on the
+    # construction step's masses (every row)
+    rp, ci = L.losa_select_blocks(mass, w.N, w.block, w.bk, w.tau)
+    rr, rh = L.losa_block_recall(mass, w.N, w.block, w.bk, rp, ci)
+    kk = 1000
+    rk, ck = L.losa_select_blocks_topk(mass, w.N, w.block, w.bk, kk)
+    torch.cuda.synchronize()
+    rp_g = rp.cpu().numpy().astype(np.int64)
+    ci_g = ci[:int(rp_g[-1])].cpu().numpy().astype(np.int64)
+    assert np.abs(f64(rr) - O.recall_rows(mg.reshape(mass.shape), rp_g, ci_g)).max() <= 1e-6
+    rk_g = rk.cpu().numpy().astype(np.int64)
+    ck_g = ck[:int(rk_g[-1])].cpu().numpy().astype(np.int64)
+    for r in range(n_q):
+        want = O.select_row_topk(mg[r], kk, n_kv, r * w.block < w.N).omega
+        assert np.array_equal(ck_g[rk_g[r]:rk_g[r + 1]], want), r
 
 
 @pytest.mark.parametrize("alpha", W.SWEEP_ALPHAS)
