@@ -450,12 +450,19 @@ def test_deterministic(L, key):
 # the frozen support is checked at the reuse steps of the measurement: Wan and
 # CogVideoX shapes at steps 0, 1, 25, 49; HunyuanVideo at 0, 1, 49
 FULL_STEPS = {"wan": (0, 1, 25, 49), "cog": (0, 1, 25, 49), "hunyuan": (0, 1, 49),
-              "wan-c32": (0, 1, 49), "hunyuan-c32": (0, 1)}
+              "wan-c32": (0, 1, 49), "hunyuan-c32": (0, 1), "wan-b2": (0, 1)}
 
 
-@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32", "hunyuan-c32"])
+@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32", "hunyuan-c32", "wan-b2"])
 def test_full_size_sampled(L, key):
-    w = (W.rectangular(W.WORKLOADS[key[:-4]]) if key.endswith("-c32") else W.WORKLOADS[key])
+    # wan-b2: the Wan shape with a batch of two (the two classifier-free guidance
+    # branches of a step are batch entries b = 0, 1, each with its own support)
+    if key.endswith("-c32"):
+        w = W.rectangular(W.WORKLOADS[key[:-4]])
+    elif key.endswith("-b2"):
+        w = W.scaled(W.WORKLOADS[key[:-3]], B=2, name="wan-b2")
+    else:
+        w = W.WORKLOADS[key]
     steps = FULL_STEPS[key]
     info = run_case(L, w, w.tau, reuse=max(steps), rows=sample_rows(w), label=f"full-{key}",
                     check_steps=steps)
