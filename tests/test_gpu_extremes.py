@@ -132,3 +132,45 @@ def test_extreme_softmax(L, case):
                       + 2.0 ** -8 * (np.abs(od_ref[:, :, :N]) + vmax) + score_term)
     else:
         assert errc.max() <= 1e-4 * max(1.0, vmax / 4) + score_term
+
+
+@pytest.mark.parametrize("dtype,scale", [("bf16", 0.02), ("bf16", 1.0), ("f32", 0.02), ("f32", 0.5)])
+def test_explicit_scale(L, dtype, scale):
+    """A score scale other than 1/sqrt(d), passed through every entry point."""
+    B, H, d, Cq, Ck, N = 1, 2, 64, 128, 32, 450
+    print(f"[gpu-extremes] scale {scale} {dtype}", flush=True)
+    rng = np.random.default_rng(9100 + int(scale * 100))
+    Np = O.padded_len(N, Cq, Ck)
+    t = torch.from_numpy(rng.standard_normal((3, B, H, Np, d))).float()
+    t[:, :, :, N:] = 0
+    t = t.to(torch.bfloat16 if dtype == "bf16" else torch.float32).cuda()
+    q, k, v = t[0].contiguous(), t[1].contiguous(), t[2].contiguous()
+    qh, kh, vh = f64(q), f64(k), f64(v)
+    n_k = Np // Ck
+    n_q = Np // Cq
+    n_kv = O.num_valid_key_blocks(N, Ck)
+    m_ref, l_ref = O.block_masses(qh, kh, N, Cq, Ck, scale)
+    mass, lse = L.losa_calibrate_mass(q, k, N, Cq, Ck, scale=scale)
+    torch.cuda.synchronize()
+    assert np.abs(f64(mass) - m_ref).max() <= 1e-4
+    assert np.abs(f64(lse)[:, :, :N] - l_ref[:, :, :N]).max() <= 1e-3
+    rp, ci = L.losa_select_blocks(mass, N, Cq, Ck, 0.9)
+    torch.cuda.synchronize()
+    rp_g = rp.cpu().numpy().astype(np.int64)
+    ci_g = ci[:int(rp_g[-1])].cpu().numpy().astype(np.int64)
+    gflat = f64(mass).reshape(-1, n_k)
+    t32 = float(np.float32(0.9))
+    for r in range(gflat.shape[0]):
+        want = O.select_row(gflat[r], t32, n_kv, (r % n_q) * Cq < N).omega
+        assert np.array_equal(ci_g[rp_g[r]:rp_g[r + 1]], want)
+    o, lo = L.losa_sparse_attn_fwd(q, k, v, N, Cq, Ck, rp, ci, scale=scale, want_lse=True)
+    oc, mc = L.losa_construct(q, k, v, N, Cq, Ck, scale=scale)
+    torch.cuda.synchronize()
+    o_ref, lo_ref = O.sparse_attention(qh, kh, vh, N, Cq, Ck, scale, rp_g, ci_g)
+    od_ref, _ = O.dense_attention(qh, kh, vh, N, scale)
+    tol = (2e-2, 2e-3) if dtype == "bf16" else (1e-4, 1e-4)
+    for got, ref in ((f64(o), o_ref), (f64(oc), od_ref)):
+        err = np.abs(got[:, :, :N] - ref[:, :, :N])
+        assert err.max() <= tol[0] and err.mean() <= tol[1]
+    assert np.abs(f64(lo)[:, :, :N] - lo_ref[:, :, :N]).max() <= 1e-3
+    assert np.abs(f64(mc) - m_ref).max() <= 1e-4
