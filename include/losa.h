@@ -86,7 +86,8 @@ typedef enum { LOSA_DTYPE_F32 = 0, LOSA_DTYPE_BF16 = 1 } losa_dtype;
  *            16 GiB.  Contents on entry are ignored and overwritten.  f32:
  *            ignored (two sweeps).
  * Arithmetic: bf16 inputs use bf16 matrix-core products with fp32
- * accumulation; f32 inputs use fp32 throughout.  Both bf16 schemes compute
+ * accumulation; f32 inputs use fp32 arithmetic, with each query's softmax
+ * normaliser carried across 32-key chunks in fp64.  Both bf16 schemes compute
  * the same scores; their masses differ only by fp32 rounding.
  */
 losa_status losa_calibrate_mass(const void* q, const void* k, losa_dtype dtype, int B, int H,
@@ -188,7 +189,8 @@ losa_status losa_block_recall(const float* mass, int B, int H, int N, int block_
  *             order, 4*B*H*n_q bytes; f32: none).
  * Arithmetic (bf16): Q K^T and P V on bf16 matrix cores with fp32
  * accumulation, softmax in fp32, P rounded to bf16 for the P V product, O
- * rounded to bf16 once at the end.  f32: fp32 throughout.
+ * rounded to bf16 once at the end.  f32: fp32 arithmetic, the softmax
+ * normaliser carried across 32-key chunks in fp64.
  */
 losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
                                  int B, int H, int N, int d, int block_q, int block_k,
