@@ -424,9 +424,10 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "bench.py measures one GPU only: every GPU box here has one "
-                          "GPU; the LoSA path shards by (batch, head) with no exchange (see "
-                          "DESIGN.md), so no multi-GPU figure is produced", "n_gpus": args.gpus}),
+        print(json.dumps({"error": "bench.py measures one GPU only: the LoSA path is built and "
+                          "timed on a single MI355X; it would shard by (batch, head) with no "
+                          "exchange between GPUs, so no multi-GPU figure is produced",
+                          "n_gpus": args.gpus}),
               flush=True)
         sys.exit(2)
 
