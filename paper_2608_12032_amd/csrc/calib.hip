@@ -130,6 +130,83 @@ __device__ __forceinline__ float tile_sums(const f32x16_t* s, float c, float m, 
   return l;
 }
 
+// tile_scores + tile_sums of a full tile in one interleaved stream, for d = 64:
+// the sub-blocks' S^T accumulate one after the other, and the exponentials of
+// sub-block kb-1 run under the MFMAs of sub-block kb.  At d = 64 a tile has
+// half the MFMAs per exponential of d = 128, and leaving them to the other
+// wave of the SIMD left the matrix cores idle (the interleave is 7-12 % faster
+// there; at d = 128 it was 5 % slower, so d = 128 keeps the two-step form).
+// Same scores, same summation order: bitwise the result of the two-step form.
+template <int D, int BLK, int TB>
+__device__ __forceinline__ float tile_fused(const char* buf, const bf16x8_t* qreg, int l32, int g,
+                                            f32x16_t* sacc, float c, float m, float* bs) {
+  using C = CalCfg<D, BLK>;
+  constexpr int KB = C::KB;
+  constexpr int SPB = KB / TB;
+  constexpr int PM = 16 / C::KS;  // scores of the previous sub-block per MFMA
+  const int ksw = l32 % C::KCH;
+  float acc[KB];
+#pragma unroll
+  for (int kb = 0; kb <= KB; ++kb) {
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) {
+      if (kb < KB) {
+        const int off = (((2 * s + g) ^ ksw) << 4);
+        const bf16x8_t a =
+            *reinterpret_cast<const bf16x8_t*>(buf + (kb * 32 + l32) * C::KROW + off);
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            a, qreg[s], s == 0 ? f32x16_t{} : sacc[kb], 0, 0, 0);
+      }
+      if (kb > 0) {
+#pragma unroll
+        for (int u = 0; u < PM; ++u) {
+          const int t = s * PM + u;
+          const float p = fast_exp2(__builtin_fmaf(sacc[kb - 1][t], c, -m));
+          acc[kb - 1] = (t == 0) ? p : acc[kb - 1] + p;
+        }
+      }
+    }
+  }
+  // per MFMA: its operand read, the MFMA, then PM (fma, add) pairs and PM exp
+#pragma unroll
+  for (int kb = 0; kb <= KB; ++kb)
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) {
+      if (kb < KB) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      if (kb > 0) {
+        __builtin_amdgcn_sched_group_barrier(0x002, 2 * PM, 0);
+        __builtin_amdgcn_sched_group_barrier(0x400, PM, 0);
+      }
+    }
+  float l = 0.f;
+#pragma unroll
+  for (int b = 0; b < TB; ++b) {
+    bs[b] = acc[b * SPB];
+#pragma unroll
+    for (int u = 1; u < SPB; ++u) bs[b] += acc[b * SPB + u];
+    l += bs[b];
+  }
+  return l;
+}
+
+// Scores of tile `buf` (keys >= kvalid masked) and this lane's probability sums
+// against m: per key block into bs, the lane's tile sum returned.
+template <int D, int BLK, int TB>
+__device__ __forceinline__ float tile_probs(const char* buf, const bf16x8_t* qreg, int l32, int g,
+                                            int kvalid, float c, float m, f32x16_t* sacc,
+                                            float* bs) {
+  using C = CalCfg<D, BLK>;
+  if constexpr (D == 64) {
+    if (kvalid == BLK) return tile_fused<D, BLK, TB>(buf, qreg, l32, g, sacc, c, m, bs);
+  }
+  tile_scores<D, BLK>(buf, qreg, l32, g, sacc);
+  if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
+  return tile_sums<C::KB, TB>(sacc, c, m, bs);
+}
+
 // Bound on one lane's tile sum (so on each probability) before the running
 // max must be raised: the max used trails the true one by at most 20 (log2
 // units), and l stays far from fp32 overflow (2^20 per key, at most 2^19 keys).
@@ -204,15 +281,13 @@ __global__ void __launch_bounds__(BLK * 2, 2)
       }
     }
     f32x16_t sacc[C::KB];
-    tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
-    if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
     // Probabilities against the running max, without looking at this tile's
     // scores first.  If a lane's tile sum exceeds the bound (or is inf: the
     // first tile), the max is raised to the tile's and the sums redone; both
     // lanes of a query take the same max, so their sums stay comparable.
     float bs[TB];
-    float lsum = tile_sums<C::KB, TB>(sacc, scale_log2, m_run, bs);
+    float lsum = tile_probs<D, BLK, TB>(cur, qreg, l32, g, kvalid, scale_log2, m_run, sacc, bs);
     if (__ballot(!(lsum <= kCalSumBound)) != 0) {
       float mx = sacc[0][0];
 #pragma unroll
@@ -256,11 +331,9 @@ __global__ void __launch_bounds__(BLK * 2, 2)
     wait_vm_barrier<0>();
     if (j + 1 < n_kv) issue_tile<D, BLK>(nxt, krs, j + 1, w, lane);
     f32x16_t sacc[C::KB];
-    tile_scores<D, BLK>(cur, qreg, l32, g, sacc);
     const int kvalid = min(BLK, N - j * BLK);
-    if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
     float acc[TB];
-    tile_sums<C::KB, TB>(sacc, scale_log2, sub, acc);
+    tile_probs<D, BLK, TB>(cur, qreg, l32, g, kvalid, scale_log2, sub, sacc, acc);
 #pragma unroll
     for (int b = 0; b < TB; ++b) {
       const float a = wave_sum(acc[b]);
