@@ -232,19 +232,21 @@ def test_calibration_schemes_and_head_groups(L, key):
     assert np.all(np.isneginf(f64(l1)[:, :, n:])) and np.all(np.isneginf(f64(l2)[:, :, n:]))
 
 
-def test_construct_full_size_wan_sampled(L):
-    w = W.WORKLOADS["wan"]
+@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32"])
+def test_construct_full_size_sampled(L, key):
+    w = W.rectangular(W.WORKLOADS[key[:-4]]) if key.endswith("-c32") else W.WORKLOADS[key]
     q, k, v = W.make_inputs(w, device="cuda")
-    o, mass = L.losa_construct(q, k, v, w.N, w.block)
+    o, mass = L.losa_construct(q, k, v, w.N, w.block, w.bk)
     torch.cuda.synchronize()
     n_q = w.n_blocks
     heads, blocks = (0, w.H - 1), (0, n_q // 2, n_q - 1)
     rows = [h * n_q + i for h in heads for i in blocks]
     qh, kh, vh = f64(q), f64(k), f64(v)
-    m_ref, _ = O.block_masses(qh, kh, w.N, w.block, w.block, w.scale, rows_subset=rows)
-    rp_full = np.arange(0, (w.H * n_q + 1) * n_q, n_q)
-    ci_full = np.tile(np.arange(n_q), w.H * n_q)
-    o_ref, _ = O.sparse_attention(qh, kh, vh, w.N, w.block, w.block, w.scale, rp_full, ci_full,
+    m_ref, _ = O.block_masses(qh, kh, w.N, w.block, w.bk, w.scale, rows_subset=rows)
+    n_kv = O.num_valid_key_blocks(w.N, w.bk)  # dense attention: every valid key block
+    rp_full = np.arange(0, (w.H * n_q + 1) * n_kv, n_kv)
+    ci_full = np.tile(np.arange(n_kv), w.H * n_q)
+    o_ref, _ = O.sparse_attention(qh, kh, vh, w.N, w.block, w.bk, w.scale, rp_full, ci_full,
                                   rows_subset=rows)
     mg, og = f64(mass), f64(o)
     for r in rows:
