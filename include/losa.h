@@ -24,8 +24,9 @@
  *   asynchronously; outputs are valid once the stream has reached that point.
  *   No call allocates, synchronizes or enqueues a memset, and each launches
  *   only on `stream`, so calls can be captured into a HIP graph and replayed
- *   (done for losa_construct, losa_select_blocks and losa_sparse_attn_fwd;
- *   losa_calibrate_mass also sets its kernel's dynamic LDS size on the host).
+ *   (tested for losa_construct, losa_select_blocks, losa_select_blocks_topk,
+ *   losa_sparse_attn_fwd and both losa_calibrate_mass schemes, which also set
+ *   their kernel's dynamic LDS size on the host).
  * - Validation is synchronous and happens before any HIP call: on an error
  *   nothing is launched, outputs are untouched, and losa_last_error() holds a
  *   description.  Launch failures return LOSA_ERR_HIP.
