@@ -402,14 +402,19 @@ def recall_heads(mbar, row_ptr, col_idx, N: int, block_q: int) -> np.ndarray:
 
 
 def recall(mbar, row_ptr, col_idx, N: int, block_q: int) -> float:
-    """Eq. (2) with M(i, j) = R_i * mbar(i, j) (R_i = valid rows of block i)."""
+    """Eq. (2) over all heads together, with M(i, j) = R_i * mbar(i, j) (R_i =
+    valid rows of block i).  Omega_i is a set of key blocks: a repeated id
+    counts once, and an id outside [0, n_k) names no block and is ignored."""
     mbar = np.asarray(mbar, dtype=np.float64)
     B, H, n_q, n_k = mbar.shape
     Ri = np.array([valid_rows(i, block_q, N).size for i in range(n_q)], dtype=np.float64)
     M = mbar * Ri[None, None, :, None]
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    col_idx = np.asarray(col_idx, dtype=np.int64)
     kept = 0.0
     flat = M.reshape(B * H * n_q, n_k)
     for r in range(B * H * n_q):
-        js = np.asarray(col_idx[row_ptr[r]:row_ptr[r + 1]], dtype=np.int64)
-        kept += flat[r, np.unique(js)].sum()
+        js = np.unique(col_idx[row_ptr[r]:row_ptr[r + 1]])
+        js = js[(js >= 0) & (js < n_k)]
+        kept += flat[r, js].sum()
     return kept / M.sum()

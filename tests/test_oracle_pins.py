@@ -392,7 +392,11 @@ def check_recall_closed_form(seed=18) -> bool:
     Ri = np.array([min(R, N - i * R) for i in range(n_q)], dtype=float)
     heads = O.recall_heads(mbar, rp, ci, N, R)
     want_h = [(np.array(want[h * n_q:(h + 1) * n_q]) * Ri).sum() / N for h in range(2)]
-    return bool(np.allclose(heads[0], want_h, rtol=0, atol=1e-12))
+    if not np.allclose(heads[0], want_h, rtol=0, atol=1e-12):
+        return False
+    # Eq. (2) over both heads at once: every head's queries carry N in total
+    total = O.recall(mbar, rp, ci, N, R)
+    return bool(abs(total - sum(want_h) / 2) <= 1e-12)
 
 
 def test_recall_closed_form_uniform_attention():
@@ -616,6 +620,13 @@ def _recall_rows_counts_duplicates(mbar, row_ptr, col_idx):
     return out
 
 
+def _recall_ids_wrap(mbar, row_ptr, col_idx, N, block_q):
+    # a negative block id taken modulo n_k instead of being ignored
+    n_k = np.asarray(mbar).shape[-1]
+    ci = np.asarray(col_idx, dtype=np.int64)
+    return _orig_recall(mbar, row_ptr, np.where(ci < 0, ci % n_k, ci), N, block_q)
+
+
 def _recall_heads_unweighted(mbar, row_ptr, col_idx, N, block_q):
     B, H, n_q, _ = np.asarray(mbar).shape
     return O.recall_rows(mbar, row_ptr, col_idx).reshape(B, H, n_q).mean(axis=2)
@@ -629,6 +640,7 @@ _orig_sparse = O.sparse_attention
 _orig_masses = O.block_masses
 _orig_select_row = O.select_row
 _orig_topk = O.select_row_topk
+_orig_recall = O.recall
 
 ALL_PINS = [check_golden, check_dense_vs_sdpa, check_sparse_full_equals_dense,
             check_masses_brute_force, check_selection_brute_force,
@@ -662,6 +674,7 @@ def _some_pin_fails():
     ("select_row_topk", _topk_off_by_one),
     ("recall_rows", _recall_rows_counts_duplicates),
     ("recall_heads", _recall_heads_unweighted),
+    ("recall", _recall_ids_wrap),
 ])
 def test_planted_mistake_is_caught(monkeypatch, attr, mutant):
     assert not _some_pin_fails(), "pins must hold for the unmodified oracle"
