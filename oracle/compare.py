@@ -33,7 +33,7 @@ def compare_selection(row_ptr, col_idx, details, mbar_ref, tau: float,
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     col_idx = np.asarray(col_idx, dtype=np.int64)
     mflat = np.asarray(mbar_ref, dtype=np.float64).reshape(len(details), -1)
-    n_exact = n_exempt = 0
+    n_exact = n_exempt = n_tie = 0
     for r, det in enumerate(details):
         got = col_idx[row_ptr[r]:row_ptr[r + 1]]
         if got.size > 1 and np.any(np.diff(got) <= 0):
@@ -51,6 +51,7 @@ def compare_selection(row_ptr, col_idx, details, mbar_ref, tau: float,
         cprev = np.concatenate([[0.0], cum[:-1]])
         boundary_mass = mflat[r, det.order[det.s - 1]]
         diff = np.setxor1d(got, want)
+        tie_used = False
         for j in diff:
             rr = rank[j]
             near_tau = (cprev[rr] <= tau + eps) and (cum[rr] >= tau - eps)
@@ -58,10 +59,14 @@ def compare_selection(row_ptr, col_idx, details, mbar_ref, tau: float,
             if not (near_tau or near_tie):
                 return dict(ok=False, row=r, reason=f"block {int(j)} differs and is not exempt",
                             got=got.tolist(), want=want.tolist())
+            tie_used |= not near_tau
         if mflat[r, got].sum() < tau - eps:
             return dict(ok=False, row=r, reason="kept mass below tau - eps")
         n_exempt += 1
-    return dict(ok=True, rows=len(details), exact=n_exact, exempt=n_exempt)
+        n_tie += tie_used
+    # exempt = rows that differ, all within the exemptions; tie_rows = those
+    # among them that needed the near-tie rule (not only the cumulative one)
+    return dict(ok=True, rows=len(details), exact=n_exact, exempt=n_exempt, tie_rows=n_tie)
 
 
 def output_errors(o_test, o_ref, N: int):

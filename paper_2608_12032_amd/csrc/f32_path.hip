@@ -51,10 +51,13 @@ __global__ void __launch_bounds__(BLK)
   const size_t head = (size_t)bh * n_pad * D;
   const int qrow = i * BLK + t;
 
+  // padding query rows take Q = 0: their scores stay finite whatever the
+  // padding holds (their output is written as 0 at the end)
+  const bool qvalid = qrow < N;
   float q[D], o[D];
 #pragma unroll
   for (int dd = 0; dd < D; ++dd) {
-    q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
+    q[dd] = qvalid ? Q[head + (size_t)qrow * D + dd] * scale_log2 : 0.f;
     o[dd] = 0.f;
   }
   float m = kNegBig;
@@ -110,7 +113,7 @@ __global__ void __launch_bounds__(BLK)
     }
   }
   const float lf = (float)l;
-  const bool ok = (qrow < N) && (lf > 0.f);
+  const bool ok = qvalid && (lf > 0.f);
   const float inv = ok ? 1.0f / lf : 0.f;
 #pragma unroll
   for (int dd = 0; dd < D; ++dd) O[head + (size_t)qrow * D + dd] = o[dd] * inv;
@@ -138,9 +141,12 @@ __global__ void __launch_bounds__(BLK)
     if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = -INFINITY;
     return;
   }
+  // padding query rows take Q = 0 (finite scores whatever the padding holds;
+  // they are never read into a mass)
+  const bool qvalid = qrow < N;
   float q[D];
 #pragma unroll
-  for (int dd = 0; dd < D; ++dd) q[dd] = Q[head + (size_t)qrow * D + dd] * scale_log2;
+  for (int dd = 0; dd < D; ++dd) q[dd] = qvalid ? Q[head + (size_t)qrow * D + dd] * scale_log2 : 0.f;
   const int n_kv = (N + BK - 1) / BK;  // key blocks holding a real key
 
   // sweep 1: running max / sum over every valid key
@@ -171,7 +177,6 @@ __global__ void __launch_bounds__(BLK)
       l += (double)part;
     }
   }
-  const bool qvalid = qrow < N;
   const float lse2 = m + __log2f((float)l);
   if (lse != nullptr) lse[(size_t)bh * n_pad + qrow] = qvalid ? lse2 * kLn2 : -INFINITY;
   const float sub = qvalid ? lse2 : INFINITY;

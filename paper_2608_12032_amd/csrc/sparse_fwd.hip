@@ -155,15 +155,21 @@ __device__ __forceinline__ void mfma_pair(const uint32_t* ka, uint32_t kimm, con
 // running max m_run (log2 units): bf16-packed into pcur; returns their fp32 sum.
 __device__ __forceinline__ float softmax_sub(const f32x16_t& cur, float scale_log2, float m_run,
                                              bf16x8_t* pcur) {
-  float ls0 = 0.f, ls1 = 0.f;
+  f32x8_t p[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    f32x8_t p;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(cur[8 * h + e], scale_log2, -m_run));
-    pcur[h] = __builtin_convertvector(p, bf16x8_t);
+    for (int e = 0; e < 8; ++e)
+      p[h][e] = fast_exp2(__builtin_fmaf(cur[8 * h + e], scale_log2, -m_run));
+    pcur[h] = __builtin_convertvector(p[h], bf16x8_t);
+  }
+  // two interleaved sums, started from the first two terms (the same values
+  // and order as starting from +0, which the compiler cannot fold away)
+  float ls0 = p[0][0], ls1 = p[0][1];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) { if (e & 1) ls1 += p[e]; else ls0 += p[e]; }
+  for (int e = 2; e < 16; e += 2) {
+    ls0 += p[e >> 3][e & 7];
+    ls1 += p[e >> 3][(e & 7) + 1];
   }
   return ls0 + ls1;
 }
@@ -205,7 +211,6 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
   bf16x8_t ring[NPRE];
 #pragma unroll
   for (int i = 0; i < NPRE; ++i) ring[i] = read_op(i);
-  float ls0 = 0.f, ls1 = 0.f;
   f32x8_t p[2];
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
@@ -229,15 +234,19 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
     }
   }
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    pcur[h] = __builtin_convertvector(p[h], bf16x8_t);
+  for (int h = 0; h < 2; ++h) pcur[h] = __builtin_convertvector(p[h], bf16x8_t);
+  // two interleaved row sums, started from the first two terms (the same
+  // values and order as starting from +0, which the compiler cannot fold)
+  float ls0 = p[0][0], ls1 = p[0][1];
 #pragma unroll
-    for (int e = 0; e < 8; e += 2) { ls0 += p[h][e]; ls1 += p[h][e + 1]; }
+  for (int e = 2; e < 16; e += 2) {
+    ls0 += p[e >> 3][e & 7];
+    ls1 += p[e >> 3][(e & 7) + 1];
   }
   // fixed issue order: the NPRE lead reads; then per MFMA the next read, its
   // load if it has one, and either EPM (fma, exp) pairs or its share of the
-  // 8 packs and 16 sums of the second half
-  constexpr int TAIL = 24;
+  // 8 packs and 14 sums of the second half
+  constexpr int TAIL = 22;
   __builtin_amdgcn_sched_group_barrier(0x100, NPRE, 0);
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
@@ -248,7 +257,7 @@ __device__ __forceinline__ float pipeline_step(const uint32_t* ka, uint32_t kimm
       __builtin_amdgcn_sched_group_barrier(0x002, EPM, 0);  // v_fma
       __builtin_amdgcn_sched_group_barrier(0x400, EPM, 0);  // v_exp
     } else {
-      __builtin_amdgcn_sched_group_barrier(0x002, 2 * TAIL / NM, 0);  // v_cvt_pk / sums
+      __builtin_amdgcn_sched_group_barrier(0x002, (2 * TAIL + NM - 1) / NM, 0);  // packs / sums
     }
   }
   // pin the softmax results here: otherwise the compiler sinks the exp2 work
@@ -365,13 +374,16 @@ __global__ void __launch_bounds__(BLK * 2)
   const int S_real = nb * NS;
   const int S = (NS == 1) ? (S_real + R - 1) / R * R : S_real;
 
-  // this lane's query row and its Q^T operand (8 bf16 per k-step)
+  // this lane's query row and its Q^T operand (8 bf16 per k-step).  Padding
+  // rows take Q = 0, so their scores stay finite whatever the padding holds
+  // (their output is written as 0 in the epilogue).
   const int qrow = qb * BLK + w * 32 + l32;
   bf16x8_t qreg[C::KS];
   {
     const bf16x8_t* qp = reinterpret_cast<const bf16x8_t*>(Q + head + (size_t)qrow * D);
+    const bool qvalid = qrow < N;
 #pragma unroll
-    for (int st = 0; st < C::KS; ++st) qreg[st] = qp[2 * st + g];
+    for (int st = 0; st < C::KS; ++st) qreg[st] = qvalid ? qp[2 * st + g] : bf16x8_t{};
   }
   // per-lane LDS addresses of the operand reads in K slot 0 / V^T slot 0; the
   // slot and the d sub-block are immediates
@@ -465,10 +477,12 @@ __global__ void __launch_bounds__(BLK * 2)
       for (int st = 0; st < C::KS; ++st) launder(ka[st]);
       launder(va[0]);
       launder(va[1]);
-      // K sub-tile s+1 and V^T sub-tile s-1 (loaded R-1 sub-iterations ago)
-      // have landed for every wave, and every wave is done with sub-iteration
-      // s-1.  Every sub-iteration issues the same loads (past the end of the
-      // stream they fetch the last block again), so the count is exact.
+      // K sub-tile s+1 and V^T sub-tile s-1 (both issued in sub-iteration
+      // s-3, so not among the last two sub-iterations' loads that the count
+      // leaves in flight) have landed for every wave, and every wave is done
+      // with sub-iteration s-1.  Every sub-iteration issues the same loads
+      // (past the end of the stream they fetch the last block again), so the
+      // count is exact.
       wait_vm_barrier<(R - 2) * 2 * C::LPW>();
       constexpr int HV = H + R - 2;  // pass-relative index of sub-tile s+R-2
       const int jk = jn[H / NS];
@@ -555,10 +569,13 @@ __global__ void __launch_bounds__(BLK * 2)
         jn[x] = __builtin_amdgcn_readfirstlane(jf[x]);
       }
     }
-    // the last passes issued loads that nothing reads: let them land before
-    // the workgroup's LDS can be handed to another workgroup
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    // drain: P V of the last sub-tile S-1 (odd, so its probabilities are pb[1])
+    // drain: P V of the last sub-tile S-1 (odd, so its probabilities are
+    // pb[1]).  Its V^T slot was filled in sub-iteration S-3, one part by each
+    // wave, and the last barrier only covered loads up to S-4: every wave
+    // waits for all of its own loads (the later ones included, which nothing
+    // reads, so that none lands after the workgroup's LDS is handed on), then
+    // a barrier makes every wave's part visible.
+    wait_vm_barrier<0>();
     mfma_pair<D, BLK, BK, false, true>(ka, 0, qreg, sc[0], va, (uint32_t)(((S - 1) % R) * C::SUB),
                                    pb[1], oacc);
   }

@@ -10,8 +10,12 @@ up to 3, so a softmax can be so peaked that an output is one V row of size 4
 and more; its bf16 rounding alone then reaches 2^-8 |o| (half an ulp), and
 rounding P to bf16 for P V adds up to 2^-9 max|v|.  The bound used here is
 derived from that arithmetic, per element:
-    |o - o_ref| <= 1e-2 + 2^-8 (|o_ref| + max|v|)   (bf16; fp32: 1e-4),
-with the workloads' mean bound (2e-3) unchanged."""
+    |o - o_ref| <= 1e-2 + 2^-8 (|o_ref| + max|v|)   (bf16; fp32: 1e-4).
+It is asserted on every element, and beside it the workloads' own bars: max-abs
+2e-2 on every element whose exact output stays in the workloads' range
+(|o_ref| <= 1, where half an output ulp is at most 2^-9), and mean-abs 2e-3
+over all valid elements.  Only the few outputs above 1 are judged by the
+arithmetic bound alone."""
 import numpy as np
 import pytest
 import torch
@@ -70,8 +74,11 @@ def test_random_configuration(L, seed):
     def close(o, o_ref):
         err = np.abs(o[:, :, :N] - o_ref[:, :, :N])
         if dtype == "bf16":
-            bound = 1e-2 + 2.0 ** -8 * (np.abs(o_ref[:, :, :N]) + vmax)
-            return bool(np.all(err <= bound) and err.mean() <= 2e-3), err
+            mag = np.abs(o_ref[:, :, :N])
+            bound = 1e-2 + 2.0 ** -8 * (mag + vmax)
+            in_range = mag <= 1.0
+            return bool(np.all(err <= bound) and err[in_range].max(initial=0.0) <= 2e-2
+                        and err.mean() <= 2e-3), err
         return bool(err.max() <= 1e-4), err
 
     m_ref, l_ref = O.block_masses(qh, kh, N, Cq, Ck, scale)
