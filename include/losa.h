@@ -9,7 +9,9 @@
  * --------------------------------
  * - All tensor pointers are caller-owned HIP DEVICE memory (16-byte aligned)
  *   unless stated otherwise.  The library never allocates device memory and
- *   keeps no state between calls except a thread-local error string.
+ *   keeps no state between calls except a thread-local error string, and for
+ *   losa_sparse_attn_fwd_noalloc a scratch array per GPU (reserved when the
+ *   library's code is loaded on that GPU) with a table of its addresses.
  * - Q, K, V, O are contiguous [B][H][N_pad][d] in the element type `dtype`,
  *   N_pad = N rounded up to max(block_q, block_k).  Token positions n >= N
  *   are padding: as keys they never enter a softmax; as queries they are left
@@ -198,6 +200,37 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
                                  float scale, const int32_t* row_ptr, const int32_t* col_idx,
                                  int64_t col_idx_len, void* o, float* lse, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/*
+ * losa_sparse_attn_fwd for callers that cannot allocate device memory: code
+ * running under HIP graph capture that may not call hipMalloc, tight serving
+ * loops, harnesses that forbid allocation.  Same arguments, results and
+ * kernels as losa_sparse_attn_fwd (bitwise the same output), without the
+ * workspace: the bf16 forward's scratch (the transposed copy of V and the
+ * rows' dispatch order, B*H*N_pad*d*2 bytes rounded up to 256 plus 4*B*H*n_q
+ * bytes) lives in a device array the library holds, LOSA_NOALLOC_SCRATCH_BYTES
+ * per GPU, reserved on each GPU the library runs on until the process ends.
+ * Neither this call nor anything it calls allocates or frees memory.
+ *
+ * - A shape whose scratch exceeds LOSA_NOALLOC_SCRATCH_BYTES returns
+ *   LOSA_ERR_CAPACITY before anything is launched (128 MiB holds, e.g., the
+ *   Wan2.1-1.3B shape: 12 heads of 32,768 x 128; use losa_sparse_attn_fwd
+ *   with a workspace for larger ones).
+ * - The scratch of the current device is used; `stream` (if not NULL) must
+ *   belong to that device, else LOSA_ERR_HIP.  The first call on a device
+ *   looks up that device's copy of the array (a host-side table, no device
+ *   memory); later calls reuse it.
+ * - Every call on one GPU shares that GPU's scratch.  Calls that overlap in
+ *   time on one GPU (other streams, or other host threads without ordering)
+ *   race on it and give undefined results; order them on one stream.
+ * - fp32 needs no scratch and runs exactly as losa_sparse_attn_fwd.
+ */
+#define LOSA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+losa_status losa_sparse_attn_fwd_noalloc(const void* q, const void* k, const void* v,
+                                         losa_dtype dtype, int B, int H, int N, int d,
+                                         int block_q, int block_k, float scale,
+                                         const int32_t* row_ptr, const int32_t* col_idx,
+                                         int64_t col_idx_len, void* o, float* lse, void* stream);
 
 /*
  * The construction step (Sec. 4.1; Sec. 5.1: one dense attention step that also

@@ -20,7 +20,8 @@ OUT = os.path.join(PKG, "liblosa.so")
 OBJDIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["calib.hip", "select.hip", "sparse_fwd.hip", "f32_path.hip", "recall.hip", "abi.cpp"]
+SOURCES = ["calib.hip", "select.hip", "sparse_fwd.hip", "f32_path.hip", "recall.hip",
+           "noalloc.hip", "abi.cpp"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

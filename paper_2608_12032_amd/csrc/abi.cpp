@@ -10,6 +10,9 @@
 
 #include "launch.hpp"
 
+static_assert(LOSA_NOALLOC_SCRATCH_BYTES == losa::kNoAllocScratchBytes,
+              "the header and the library agree on the no-alloc scratch size");
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -260,29 +263,48 @@ losa_status losa_block_recall(const float* mass, int B, int H, int N, int block_
                     "losa_block_recall");
 }
 
-losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
-                                 int B, int H, int N, int d, int block_q, int block_k,
-                                 float scale, const int32_t* row_ptr, const int32_t* col_idx,
-                                 int64_t col_idx_len, void* o, float* lse, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the sparse forward (both entry points).  Fills `s`.
+losa_status fwd_checks(const void* q, const void* k, const void* v, losa_dtype dtype, int B, int H,
+                       int N, int d, int block_q, int block_k, float scale,
+                       const int32_t* row_ptr, const int32_t* col_idx, int64_t col_idx_len,
+                       const void* o, const float* lse, Shape* s) {
   if (!q || !k || !v || !row_ptr || !o)
     return fail(LOSA_ERR_NULL_POINTER, "q, k, v, row_ptr and o must be non-NULL");
   if (col_idx_len < 0) return fail(LOSA_ERR_INVALID_SHAPE, "col_idx_len must be >= 0");
   if (col_idx_len > 0 && !col_idx)
     return fail(LOSA_ERR_NULL_POINTER, "col_idx is NULL but col_idx_len > 0");
-  Shape s;
-  losa_status st = check_shape(B, H, N, d, block_q, block_k, &s);
+  losa_status st = check_shape(B, H, N, d, block_q, block_k, s);
   if (st != LOSA_OK) return st;
   if (!std::isfinite(scale) || !(scale > 0.f))
     return fail(LOSA_ERR_INVALID_SHAPE, "scale must be finite and > 0");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
       (lse && !aligned16(lse)) || !aligned16(row_ptr) || (col_idx && !aligned16(col_idx)))
     return fail(LOSA_ERR_ALIGNMENT, "pointers must be 16-byte aligned");
-  st = check_supported(dtype, s);
+  st = check_supported(dtype, *s);
   if (st != LOSA_OK) return st;
-  if (s.n_k > losa::kSparseFwdMaxNk)
-    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per head exceeds %d", s.n_k,
+  if (s->n_k > losa::kSparseFwdMaxNk)
+    return fail(LOSA_ERR_UNSUPPORTED, "n_k=%d key blocks per head exceeds %d", s->n_k,
                 losa::kSparseFwdMaxNk);
+  return LOSA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, losa_dtype dtype,
+                                 int B, int H, int N, int d, int block_q, int block_k,
+                                 float scale, const int32_t* row_ptr, const int32_t* col_idx,
+                                 int64_t col_idx_len, void* o, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  Shape s;
+  losa_status st = fwd_checks(q, k, v, dtype, B, H, N, d, block_q, block_k, scale, row_ptr,
+                              col_idx, col_idx_len, o, lse, &s);
+  if (st != LOSA_OK) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (dtype == LOSA_DTYPE_BF16) {
     const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q);
@@ -298,6 +320,44 @@ losa_status losa_sparse_attn_fwd(const void* q, const void* k, const void* v, lo
   return hip_status(losa::launch_sparse_fwd_f32(d, block_q, block_k, q, k, v, B, H, N, s.n_pad, scale,
                                                 row_ptr, col_idx, col_idx_len, o, lse, hs),
                     "losa_sparse_attn_fwd");
+}
+
+losa_status losa_sparse_attn_fwd_noalloc(const void* q, const void* k, const void* v,
+                                         losa_dtype dtype, int B, int H, int N, int d, int block_q,
+                                         int block_k, float scale, const int32_t* row_ptr,
+                                         const int32_t* col_idx, int64_t col_idx_len, void* o,
+                                         float* lse, void* stream) {
+  Shape s;
+  losa_status st = fwd_checks(q, k, v, dtype, B, H, N, d, block_q, block_k, scale, row_ptr,
+                              col_idx, col_idx_len, o, lse, &s);
+  if (st != LOSA_OK) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (dtype == LOSA_DTYPE_BF16) {
+    const size_t need = losa::sparse_fwd_bf16_workspace(B, H, s.n_pad, d, s.n_q);
+    if (need > losa::kNoAllocScratchBytes)
+      return fail(LOSA_ERR_CAPACITY,
+                  "losa_sparse_attn_fwd_noalloc: this shape needs %zu bytes of scratch, more than "
+                  "the %zu the library holds; use losa_sparse_attn_fwd with a workspace",
+                  need, losa::kNoAllocScratchBytes);
+    void* ws = nullptr;
+    int dev = -1;
+    const hipError_t e = losa::noalloc_scratch(hs, &ws, &dev);
+    if (e == hipErrorInvalidResourceHandle)
+      return fail(LOSA_ERR_HIP,
+                  "losa_sparse_attn_fwd_noalloc: the stream belongs to another device than the "
+                  "current device %d",
+                  dev);
+    st = hip_status(e, "losa_sparse_attn_fwd_noalloc (scratch lookup)");
+    if (st != LOSA_OK) return st;
+    return hip_status(losa::launch_sparse_fwd_bf16(d, block_q, block_k, q, k, v, B, H, N,
+                                                   s.n_pad, scale, row_ptr, col_idx, col_idx_len,
+                                                   o, lse, ws, hs),
+                      "losa_sparse_attn_fwd_noalloc");
+  }
+  // fp32 needs no scratch: the same kernel as losa_sparse_attn_fwd
+  return hip_status(losa::launch_sparse_fwd_f32(d, block_q, block_k, q, k, v, B, H, N, s.n_pad,
+                                                scale, row_ptr, col_idx, col_idx_len, o, lse, hs),
+                    "losa_sparse_attn_fwd_noalloc");
 }
 
 losa_status losa_construct(const void* q, const void* k, const void* v, losa_dtype dtype, int B,

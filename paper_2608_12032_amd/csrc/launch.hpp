@@ -68,4 +68,13 @@ size_t recall_workspace_bytes(int rows);
 // workgroup keeps one flag per key block of its row in LDS.
 constexpr int kSparseFwdMaxNk = 4096;
 
+// Scratch held by the library for losa_sparse_attn_fwd_noalloc (a device
+// array per GPU, noalloc.hip).  Must equal LOSA_NOALLOC_SCRATCH_BYTES.
+constexpr size_t kNoAllocScratchBytes = (size_t)128 << 20;
+// Device address of the current device's copy of the scratch array, looked up
+// once per device.  Fails with hipErrorInvalidResourceHandle if `stream`
+// (non-null) belongs to another device than the current one; `device`
+// receives the current device.
+hipError_t noalloc_scratch(hipStream_t stream, void** ptr, int* device);
+
 }  // namespace losa

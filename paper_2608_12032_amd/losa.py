@@ -23,8 +23,12 @@ STATUS = {0: "LOSA_OK", 1: "LOSA_ERR_NULL_POINTER", 2: "LOSA_ERR_INVALID_SHAPE",
           6: "LOSA_ERR_CAPACITY", 7: "LOSA_ERR_HIP"}
 
 EXPORTED = ("losa_calibrate_mass", "losa_select_blocks", "losa_select_blocks_topk",
-            "losa_block_recall", "losa_sparse_attn_fwd", "losa_construct", "losa_workspace_bytes",
-            "losa_status_string", "losa_last_error", "losa_version")
+            "losa_block_recall", "losa_sparse_attn_fwd", "losa_sparse_attn_fwd_noalloc",
+            "losa_construct", "losa_workspace_bytes", "losa_status_string", "losa_last_error",
+            "losa_version")
+
+# bytes of library-held scratch behind losa_sparse_attn_fwd_noalloc (per GPU)
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class LosaError(RuntimeError):
@@ -48,6 +52,9 @@ def _load():
     lib.losa_block_recall.restype = I
     lib.losa_sparse_attn_fwd.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, L, P, P, P, Z, P]
     lib.losa_sparse_attn_fwd.restype = I
+    lib.losa_sparse_attn_fwd_noalloc.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, L, P, P,
+                                                 P]
+    lib.losa_sparse_attn_fwd_noalloc.restype = I
     lib.losa_construct.argtypes = [P, P, P, I, I, I, I, I, I, I, F, P, P, P, P, Z, P]
     lib.losa_construct.restype = I
     lib.losa_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
@@ -286,6 +293,34 @@ def losa_sparse_attn_fwd(q, k, v, N: int, block_q: int, block_k: int | None, row
     return (o, lse) if want_lse else o
 
 
+def losa_sparse_attn_fwd_noalloc(q, k, v, N: int, block_q: int, block_k: int | None, row_ptr,
+                                 col_idx, scale: float | None = None, want_lse: bool = False,
+                                 out=None, lse=None):
+    """losa_sparse_attn_fwd without a workspace: the library's own scratch
+    (NOALLOC_SCRATCH_BYTES per GPU) holds it.  Allocates only the outputs
+    that are not given; pass ``out`` (and ``lse``) to allocate nothing."""
+    block_k = block_k or block_q
+    B, H, Np, d = _qkv(q, {"k": k, "v": v}, N, block_q, block_k)
+    dev = q.device
+    _arg(row_ptr, "row_ptr", dev, dtype=torch.int32, numel=B * H * (Np // block_q) + 1)
+    _arg(col_idx, "col_idx", dev, dtype=torch.int32)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    o = torch.empty_like(q) if out is None else out
+    _arg(o, "out", dev, dtype=q.dtype, shape=q.shape)
+    if want_lse and lse is None:
+        lse = torch.empty((B, H, Np), dtype=torch.float32, device=dev)
+    if want_lse:
+        _arg(lse, "lse", dev, dtype=torch.float32, shape=(B, H, Np))
+    if torch.cuda.current_device() != dev.index:
+        raise ValueError(f"the tensors live on {dev}; make it the current device")
+    st = lib.losa_sparse_attn_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, H, N, d,
+                                          block_q, block_k, scale, _ptr(row_ptr), _ptr(col_idx),
+                                          col_idx.numel(), _ptr(o),
+                                          _ptr(lse if want_lse else None), _stream(dev))
+    _check(st, "losa_sparse_attn_fwd_noalloc")
+    return (o, lse) if want_lse else o
+
+
 def losa_construct(q, k, v, N: int, block_q: int, block_k: int | None = None,
                    scale: float | None = None, want_lse: bool = False, out=None, mass=None,
                    lse=None, workspace=None):
@@ -326,4 +361,5 @@ select_blocks = losa_select_blocks
 select_blocks_topk = losa_select_blocks_topk
 block_recall = losa_block_recall
 sparse_attn_fwd = losa_sparse_attn_fwd
+sparse_attn_fwd_noalloc = losa_sparse_attn_fwd_noalloc
 construct = losa_construct

@@ -106,6 +106,32 @@ def test_fwd_validation(L, kw, code):
     assert _fwd(L, **kw) == code
 
 
+def _fwd_na(L, q=FAKE, dtype=1, B=1, H=2, N=1000, d=128, bq=128, bk=128, rp=FAKE, ci=FAKE,
+            cl=100, o=FAKE, scale=0.1):
+    return L.lib.losa_sparse_attn_fwd_noalloc(q, q, q, dtype, B, H, N, d, bq, bk, scale, rp, ci,
+                                              cl, o, None, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), 1), (dict(rp=None), 1), (dict(o=None), 1), (dict(ci=None), 1),
+    (dict(cl=-1), 2), (dict(B=-1), 2), (dict(q=MIS), 4), (dict(d=80), 5),
+    # scratch beyond the 128 MiB the library holds: the HunyuanVideo shape's V^T
+    (dict(B=1, H=24, N=118800), 6), (dict(B=2, H=12, N=32760), 6),
+])
+def test_fwd_noalloc_validation(L, kw, code):
+    assert _fwd_na(L, **kw) == code
+    if code == 6:
+        assert "scratch" in L.lib.losa_last_error().decode()
+
+
+def test_fwd_noalloc_scratch_limit(L):
+    # the Wan shape (96 MiB of V^T plus the dispatch order) fits; 16 more
+    # heads of it do not
+    fits = L.workspace_bytes(2, 1, 1, 12, 32760, 128, 128, 128)
+    assert fits <= L.NOALLOC_SCRATCH_BYTES < L.workspace_bytes(2, 1, 1, 16, 32760, 128, 128, 128)
+    assert _fwd_na(L, H=16, N=32760) == 6
+
+
 def _topk(L, mass=FAKE, B=1, H=2, N=1000, bq=128, bk=32, k=5, rp=FAKE, ci=FAKE, cap=10**6,
           ws=FAKE, wsb=10**7):
     return L.lib.losa_select_blocks_topk(mass, B, H, N, bq, bk, k, rp, ci, cap, ws, wsb, None)
