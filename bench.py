@@ -515,9 +515,17 @@ def main():
     elt = 2 if w.dtype == "bf16" else 4
     qkv = w.B * w.H * n_pad * d * elt
     mass_b = w.B * w.H * n_q * n_k * 4
+    stat_b = w.B * w.H * n_k * n_pad * 4   # one-sweep block statistics, fp32 per (query, key block)
+    lse_b = w.B * w.H * n_pad * 4
     alg = {"sparse_fwd": 4 * qkv + 4 * (rows + 1 + nnz),
-           "calibrate": 2 * qkv + mass_b,
+           # one sweep (the timed scheme): Q, K read; statistics and lse written
+           # by the sweep and read back by the reduction; masses written
+           "calibrate": 2 * qkv + 2 * stat_b + 2 * lse_b + mass_b,
+           # two sweeps: Q, K read, masses written (the second sweep's re-reads
+           # of K are not algorithmic)
+           "calibrate_two_sweep": 2 * qkv + mass_b,
            "select": mass_b + 4 * (rows + 1 + nnz)}
+    qk_flop = 2.0 * w.B * w.H * n_pad * n_pad * d   # one Q K^T over every (query, key) pair
     con_t = sum(con_ms) / len(con_ms)
     sel_t = sum(sel_ms) / len(sel_ms)
 
@@ -590,10 +598,18 @@ def main():
                                     "mean": round(float(rh_k.float().mean()), 5),
                                     "worst_head": round(float(rh_k.float().min()), 5)}}
     del rp_k, ci_k, ws_cal
-    hbm = {"calibrate": {"algorithmic_GBs": round(alg["calibrate"] / cal_t / 1e6, 1)},
+    hbm = {"calibrate": {"algorithmic_GBs": round(alg["calibrate"] / cal_t / 1e6, 1),
+                         "qk_tflops": round(qk_flop / (cal_t * 1e-3) / 1e12, 1),
+                         "qk_frac_of_mfma_peak": round(qk_flop / (cal_t * 1e-3) / 1e12
+                                                       / MFMA_BF16_PEAK_TFLOPS, 4)},
+           "calibrate_two_sweep": {"algorithmic_GBs": round(alg["calibrate_two_sweep"] / cal2_t
+                                                            / 1e6, 1),
+                                   "qk_tflops": round(2 * qk_flop / (cal2_t * 1e-3) / 1e12, 1)},
            "select": {"algorithmic_GBs": round(alg["select"] / sel_t / 1e6, 1)},
            "note": "algorithmic bytes / measured time; counted_GBs = rocprofv3 FETCH_SIZE + "
-                   "WRITE_SIZE bytes (scaled by a reference copy) / measured time"}
+                   "WRITE_SIZE bytes (scaled by a reference copy) / measured time; qk_tflops "
+                   "counts one Q K^T per sweep (2 N_pad^2 d per head), the calibration's only "
+                   "matrix work"}
     if traffic:
         kb = traffic["kernels"]
         tot = lambda key: kb.get(key, {}).get("fetch_bytes", 0) + kb.get(key, {}).get("write_bytes", 0)  # noqa: E731
