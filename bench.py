@@ -36,6 +36,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix-core peak
+# fp32 inputs run on the vector ALUs (fp32 fma per thread, no matrix cores):
+# 256 CUs x 2.4 GHz x 256 FLOP/clk (128 fp32 lanes per CU, fma = 2 FLOP,
+# counting the packed two-wide fma; plain fma issue reaches half of it)
+FP32_VECTOR_PEAK_TFLOPS = 157.3
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_fwd_traffic.json")
 CSRC = os.path.join(ROOT, "paper_2608_12032_amd", "csrc")
@@ -508,6 +512,7 @@ def main():
     retained_flop = 4.0 * C * Ck * d * nnz
     dense_flop = 4.0 * w.B * w.H * N * N * d
     achieved = retained_flop / (fwd * 1e-3) / 1e12
+    peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_VECTOR_PEAK_TFLOPS
     wkey = args.workload + (f"-c{Ck}" if Ck != C else "")
     traffic = measured_traffic(wkey)
     n_pad = w.N_pad
@@ -654,11 +659,11 @@ def main():
         "dense_equiv_tflops": round(dense_flop / (fwd * 1e-3) / 1e12, 1),
         "kernel_speedup_vs_dense_flops": round(dense_flop / retained_flop, 3),
         "roofline": {
-            "bound": "mfma",
+            "bound": "mfma" if w.dtype == "bf16" else "alu",
             "achieved": round(achieved, 1),
-            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "frac": round(achieved / peak, 4),
             "traffic": traffic["bytes_per_launch"] if traffic else None,
             "traffic_algorithmic": alg["sparse_fwd"],
         },
