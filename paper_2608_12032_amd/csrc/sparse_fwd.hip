@@ -291,9 +291,20 @@ __device__ __forceinline__ void mask_sub(f32x16_t& s, int part, int kvalid, int 
 // (at most 2^20 per key over at most 2^19 keys).
 constexpr float kSumBound = 1048576.0f;
 
+// Waves per SIMD the register budget is cut for.  128-row query blocks: two at
+// d = 128 (output accumulators, Q operands and two score tiles take ~250
+// registers); three at d = 64, where a wave's VALU work per MFMA is twice that
+// of d = 128 and a third wave hides more of it (168 registers; the rings and
+// block list, 40 KiB per workgroup, allow four).  64-row blocks are limited by
+// LDS instead.
+template <int D, int BLK>
+constexpr int fwd_waves_per_simd() {
+  return BLK == 128 ? (D == 64 ? 3 : 2) : 1;
+}
+
 template <int D, int BLK, int BK, bool DENSE>
 __global__ void __launch_bounds__(BLK * 2)
-    __attribute__((amdgpu_waves_per_eu(BLK == 128 ? 2 : 1)))
+    __attribute__((amdgpu_waves_per_eu(fwd_waves_per_simd<D, BLK>())))
     sparse_fwd_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                            const __bf16* __restrict__ Vt, const int32_t* __restrict__ row_ptr,
                            const int32_t* __restrict__ col_idx, int64_t col_len,
