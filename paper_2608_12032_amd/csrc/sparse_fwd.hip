@@ -98,6 +98,7 @@ struct FwdCfg {
   static constexpr int DB = D / 32;                  // 32-row d sub-blocks of O^T
   static constexpr int NS = BK / 32;                 // 32-key sub-tiles per key block
   static constexpr int R = kRing;                    // slots per ring
+  static constexpr int LEAD = D == 64 ? 6 : 4;       // MFMAs an LDS operand read leads by
   static constexpr int BPI = R / NS;                 // key blocks per unrolled loop pass
   static constexpr int SUB = 32 * D * 2;             // bytes of a K or V^T sub-tile
   static constexpr int RING = R * SUB;               // bytes of one ring
@@ -516,7 +517,7 @@ __global__ void __launch_bounds__(BLK * 2)
       // raised wave priority while the matrix cores are fed: when both waves
       // of a SIMD have instructions ready, the one inside its MFMA stream issues
       __builtin_amdgcn_s_setprio(1);
-      float ls = pipeline_step<D, BLK, BK, 4, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
+      float ls = pipeline_step<D, BLK, BK, C::LEAD, 2 * C::LPW>(ka, ((H + 1) % R) * C::SUB, qreg, nxt, va,
                                           ((H + R - 1) % R) * C::SUB, pb[(H + 1) & 1], oacc,
                                           cur, scale_log2, m_run, pb[H & 1], issue);
       __builtin_amdgcn_s_setprio(0);
