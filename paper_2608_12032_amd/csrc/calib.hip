@@ -212,8 +212,19 @@ __device__ __forceinline__ float tile_probs(const char* buf, const bf16x8_t* qre
 // units), and l stays far from fp32 overflow (2^20 per key, at most 2^19 keys).
 constexpr float kCalSumBound = 1048576.0f;
 
+// Waves per SIMD the register budget is cut for: two at d = 128 (a 128-key
+// tile of scores and the Q operands take ~200 registers; the double-buffered
+// tiles, 64 KiB per workgroup, allow no more), four at d = 64 (128 registers;
+// 32 KiB of tiles, plus the two-sweep scheme's partials), where more waves
+// overlap the exponentials of some with the MFMAs of others.
+template <int D>
+constexpr int cal_waves_per_simd() {
+  return D == 64 ? 4 : 2;
+}
+
 template <int D, int BLK, int BK, bool STATS>
-__global__ void __launch_bounds__(BLK * 2, 2)
+__global__ void __launch_bounds__(BLK * 2)
+    __attribute__((amdgpu_waves_per_eu(cal_waves_per_simd<D>())))
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                       float* __restrict__ mass, float* __restrict__ lse,
                       float* __restrict__ stat, int rows_total, int n_q, int n_k, int N,
