@@ -44,15 +44,21 @@ namespace losa {
 
 namespace {
 
+// Keys per LDS tile: 64 at d = 128 with 128-row query blocks (a tile of scores
+// then takes 32 registers instead of 64, and two 16 KiB tiles leave LDS for
+// three workgroups per CU), else one tile per query block's worth of keys.
+constexpr int cal_tile_keys(int d, int blk) { return (d == 128 && blk == 128) ? 64 : blk; }
+
 template <int D, int BLK>
 struct CalCfg {
   static constexpr int NW = BLK / 32;
   static constexpr int NT = NW * 64;
   static constexpr int KS = D / 16;
-  static constexpr int KB = BLK / 32;                // 32-key sub-blocks of a tile
+  static constexpr int TK = cal_tile_keys(D, BLK);   // keys per tile
+  static constexpr int KB = TK / 32;                 // 32-key sub-blocks of a tile
   static constexpr int KROW = D * 2;
   static constexpr int KCH = D / 8;
-  static constexpr int TILE = BLK * D * 2;
+  static constexpr int TILE = TK * D * 2;
   static constexpr int LOADS = TILE / (1024 * NW);
   static_assert(TILE % (1024 * NW) == 0, "tile must split into whole wave loads");
 };
@@ -68,7 +74,7 @@ __device__ __forceinline__ void issue_tile(char* buf, __amdgpu_buffer_rsrc_t rs,
     const int row = o / C::KROW;
     const int pch = (o % C::KROW) >> 4;
     const int c = pch ^ (row % C::KCH);
-    load_lds_16(rs, buf + base, (uint32_t)(((j * BLK + row) * D + c * 8) * 2));
+    load_lds_16(rs, buf + base, (uint32_t)(((j * C::TK + row) * D + c * 8) * 2));
   }
 }
 
@@ -200,10 +206,10 @@ __device__ __forceinline__ float tile_probs(const char* buf, const bf16x8_t* qre
                                             float* bs) {
   using C = CalCfg<D, BLK>;
   if constexpr (D == 64) {
-    if (kvalid == BLK) return tile_fused<D, BLK, TB>(buf, qreg, l32, g, sacc, c, m, bs);
+    if (kvalid == C::TK) return tile_fused<D, BLK, TB>(buf, qreg, l32, g, sacc, c, m, bs);
   }
   tile_scores<D, BLK>(buf, qreg, l32, g, sacc);
-  if (kvalid < BLK) mask_tile<C::KB>(sacc, kvalid, g);
+  if (kvalid < C::TK) mask_tile<C::KB>(sacc, kvalid, g);
   return tile_sums<C::KB, TB>(sacc, c, m, bs);
 }
 
@@ -212,27 +218,28 @@ __device__ __forceinline__ float tile_probs(const char* buf, const bf16x8_t* qre
 // units), and l stays far from fp32 overflow (2^20 per key, at most 2^19 keys).
 constexpr float kCalSumBound = 1048576.0f;
 
-// Waves per SIMD the register budget is cut for: two at d = 128 (a 128-key
-// tile of scores and the Q operands take ~200 registers; the double-buffered
-// tiles, 64 KiB per workgroup, allow no more), four at d = 64 (128 registers;
-// 32 KiB of tiles, plus the two-sweep scheme's partials), where more waves
-// overlap the exponentials of some with the MFMAs of others.
-template <int D>
+// Waves per SIMD the register budget is cut for, so that the exponentials of
+// some waves overlap the MFMAs of others: four with 128-row query blocks or at
+// d = 64 (a 64-key tile of scores and the Q operands fit 128 registers; 32 KiB
+// of tiles per workgroup), two otherwise.  The two-sweep scheme's partials add
+// LDS and can lower the count the LDS allows.
+template <int D, int BLK>
 constexpr int cal_waves_per_simd() {
-  return D == 64 ? 4 : 2;
+  return (D == 64 || BLK == 128) ? 4 : 2;
 }
 
 template <int D, int BLK, int BK, bool STATS>
 __global__ void __launch_bounds__(BLK * 2)
-    __attribute__((amdgpu_waves_per_eu(cal_waves_per_simd<D>())))
+    __attribute__((amdgpu_waves_per_eu(cal_waves_per_simd<D, BLK>())))
     calib_bf16_kernel(const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
                       float* __restrict__ mass, float* __restrict__ lse,
                       float* __restrict__ stat, int rows_total, int n_q, int n_k, int N,
                       int n_pad, float scale_log2) {
   using C = CalCfg<D, BLK>;
-  static_assert(BK % 32 == 0 && BLK % BK == 0, "key blocks split a tile into whole sub-blocks");
-  constexpr int TB = BLK / BK;   // key blocks per tile
-  constexpr int SPB = BK / 32;   // 32-key sub-blocks per key block
+  static_assert(BK % 32 == 0 && BLK % BK == 0, "key blocks split a query block's keys");
+  static_assert(C::TK % BK == 0 || BK % C::TK == 0, "tiles and key blocks nest");
+  constexpr int TB = C::TK >= BK ? C::TK / BK : 1;   // key blocks (or parts of one) per tile
+  constexpr int TPB = BK > C::TK ? BK / C::TK : 1;   // tiles per key block
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   char* buf0 = smem;
   char* buf1 = smem + C::TILE;
@@ -270,12 +277,20 @@ __global__ void __launch_bounds__(BLK * 2)
 #pragma unroll
     for (int s = 0; s < C::KS; ++s) qreg[s] = qvalid ? qp[2 * s + g] : bf16x8_t{};
   }
-  const int n_kv = (N + BLK - 1) / BLK;  // key tiles holding a real key
+  const int n_kv = (N + C::TK - 1) / C::TK;  // key tiles holding a real key
+  // a key block's sums are complete after its last tile, or after the last
+  // tile swept (the block's remaining tiles hold no key)
+  auto block_done = [&](int j) { return TPB == 1 || j % TPB == TPB - 1 || j == n_kv - 1; };
+  auto first_block = [&](int j) { return TPB == 1 ? j * TB : j / TPB; };
 
   // ---- sweep 1: running max / sum -> lse (log2 units) ----------------------
   float m_run = kNegBig;
   float l_run = 0.f;
-  float pend[TB];  // STATS: the previous tile's block statistics, stored one tile late
+  float pend[TB];  // STATS: finished block statistics, stored one tile late
+  int pend_blk = -1;  // first key block of pend (-1: nothing pending)
+  float bacc[TB];  // block sums so far against m_run (TPB > 1: over the block's tiles)
+#pragma unroll
+  for (int b = 0; b < TB; ++b) bacc[b] = 0.f;
   issue_tile<D, BLK>(buf0, krs, 0, w, lane);
   for (int j = 0; j < n_kv; ++j) {
     char* cur = (j & 1) ? buf1 : buf0;
@@ -285,14 +300,15 @@ __global__ void __launch_bounds__(BLK * 2)
     if constexpr (STATS) {
       // the stores go out a whole tile before the next vmcnt(0) wait, which
       // then finds them done instead of waiting out their latency
-      if (j > 0 && g == 0) {
+      if (pend_blk >= 0 && g == 0) {
 #pragma unroll
         for (int b = 0; b < TB; ++b)
-          stat[((size_t)bh * n_k + (j - 1) * TB + b) * n_pad + qrow] = pend[b];
+          stat[((size_t)bh * n_k + pend_blk + b) * n_pad + qrow] = pend[b];
       }
+      pend_blk = -1;
     }
     f32x16_t sacc[C::KB];
-    const int kvalid = min(BLK, N - j * BLK);
+    const int kvalid = min(C::TK, N - j * C::TK);
     // Probabilities against the running max, without looking at this tile's
     // scores first.  If a lane's tile sum exceeds the bound (or is inf: the
     // first tile), the max is raised to the tile's and the sums redone; both
@@ -307,14 +323,23 @@ __global__ void __launch_bounds__(BLK * 2)
         for (int t = 0; t < 16; ++t) mx = fmaxf(mx, sacc[kb][t]);
       mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;  // scale > 0: max commutes with it
       const float m_new = fmaxf(m_run, mx);
-      l_run *= fast_exp2(m_run - m_new);
+      const float alpha = fast_exp2(m_run - m_new);
+      l_run *= alpha;
+      if constexpr (TPB > 1) bacc[0] *= alpha;
       m_run = m_new;
       lsum = tile_sums<C::KB, TB>(sacc, scale_log2, m_run, bs);
     }
     l_run += lsum;
-    if constexpr (STATS) {
 #pragma unroll
-      for (int b = 0; b < TB; ++b) pend[b] = __log2f(bs[b] + __shfl_xor(bs[b], 32)) + m_run;
+    for (int b = 0; b < TB; ++b) bacc[b] = TPB == 1 ? bs[b] : bacc[b] + bs[b];
+    if (block_done(j)) {
+      if constexpr (STATS) {
+#pragma unroll
+        for (int b = 0; b < TB; ++b) pend[b] = __log2f(bacc[b] + __shfl_xor(bacc[b], 32)) + m_run;
+        pend_blk = first_block(j);
+      }
+#pragma unroll
+      for (int b = 0; b < TB; ++b) bacc[b] = 0.f;
     }
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -325,7 +350,7 @@ __global__ void __launch_bounds__(BLK * 2)
     if (g == 0) {
 #pragma unroll
       for (int b = 0; b < TB; ++b)
-        stat[((size_t)bh * n_k + (n_kv - 1) * TB + b) * n_pad + qrow] = pend[b];
+        stat[((size_t)bh * n_k + pend_blk + b) * n_pad + qrow] = pend[b];
     }
     return;
   }
@@ -334,6 +359,8 @@ __global__ void __launch_bounds__(BLK * 2)
   const float sub = qvalid ? lse2 : INFINITY;
 
   // ---- sweep 2: block masses -----------------------------------------------
+#pragma unroll
+  for (int b = 0; b < TB; ++b) bacc[b] = 0.f;
   wait_vm_barrier<0>();  // all waves are done with the last tile of sweep 1 (or with nothing)
   issue_tile<D, BLK>(buf0, krs, 0, w, lane);
   for (int j = 0; j < n_kv; ++j) {
@@ -342,18 +369,24 @@ __global__ void __launch_bounds__(BLK * 2)
     wait_vm_barrier<0>();
     if (j + 1 < n_kv) issue_tile<D, BLK>(nxt, krs, j + 1, w, lane);
     f32x16_t sacc[C::KB];
-    const int kvalid = min(BLK, N - j * BLK);
+    const int kvalid = min(C::TK, N - j * C::TK);
     float acc[TB];
     tile_probs<D, BLK, TB>(cur, qreg, l32, g, kvalid, scale_log2, sub, sacc, acc);
 #pragma unroll
-    for (int b = 0; b < TB; ++b) {
-      const float a = wave_sum(acc[b]);
-      if (lane == 0) part[w * n_k + j * TB + b] = a;
+    for (int b = 0; b < TB; ++b) bacc[b] = TPB == 1 ? acc[b] : bacc[b] + acc[b];
+    if (block_done(j)) {
+      const int j0 = first_block(j);
+#pragma unroll
+      for (int b = 0; b < TB; ++b) {
+        const float a = wave_sum(bacc[b]);
+        if (lane == 0) part[w * n_k + j0 + b] = a;
+        bacc[b] = 0.f;
+      }
     }
   }
   lds_read_barrier();  // partials written (lgkmcnt covers the LDS stores)
   const float inv_rows = 1.0f / (float)rows_valid;
-  const int n_kb = n_kv * TB;  // key blocks inside the tiles swept (the rest hold no key)
+  const int n_kb = first_block(n_kv - 1) + TB;  // key blocks the sweep covered (the rest hold no key)
   for (int j = tid; j < n_k; j += C::NT) {
     float s = 0.f;
     if (j < n_kb) {
@@ -475,7 +508,7 @@ hipError_t launch_stat_mass(int blk, int blk_k, const float* stat, const float* 
 }
 
 size_t calib_bf16_lds_bytes(int d, int blk, int n_k) {
-  return 2 * (size_t)blk * d * 2 + (size_t)(blk / 32) * n_k * sizeof(float);
+  return 2 * (size_t)cal_tile_keys(d, blk) * d * 2 + (size_t)(blk / 32) * n_k * sizeof(float);
 }
 
 hipError_t launch_calibrate_bf16(int d, int blk, int blk_k, const void* q, const void* k, int B,
