@@ -4,8 +4,9 @@
 // Work unit.  One workgroup owns one CSR row r = (b*H + h)*n_q + i: the BLK
 // query rows of query block i, 32 per wave (BLK/32 waves, one per SIMD for
 // BLK = 128), and walks only the key blocks the row retains.  Two workgroups
-// share a CU, so each SIMD runs two independent waves: while one waits at its
-// workgroup barrier the other keeps the matrix core busy.  The workgroup first
+// share a CU at d = 128 and three at d = 64, so each SIMD runs two or three
+// independent waves: while one waits at its workgroup barrier or on its
+// exponentials, another keeps the matrix core busy.  The workgroup first
 // turns its CSR entries into a sorted list of distinct valid block ids in LDS
 // (per-block flags, then a ballot compaction), which realises Eq. (4)'s set
 // semantics exactly: a repeated id counts once, ids outside [0, n_k) are
@@ -30,8 +31,9 @@
 //
 // Streaming.  The row's keys are a stream of 32-key sub-tiles (NS = BK/32 per
 // key block of BK keys; with BK = 32 the stream is padded to whole loop passes
-// with sub-tiles whose keys are all masked).  K and V^T sub-tiles pass through two rings of kRing LDS slots,
-// filled by 16-byte buffer loads that write LDS directly.  Sub-iteration s
+// with sub-tiles whose keys are all masked).  K and V^T sub-tiles pass through
+// two rings of kRing LDS slots, filled by 16-byte buffer loads that write LDS
+// directly.  Sub-iteration s
 // reads K sub-tile s+1 (scores of the next sub-tile) and V^T sub-tile s-1
 // (P V of the previous one); after the barrier that opens it, the slots that
 // sub-iteration s-1 finished with are refilled with K sub-tile s+kRing and V^T
