@@ -7,7 +7,9 @@
 // i.e. Eq. (1)'s M(i, j) divided by R_i, so every row of mbar sums to one.
 // Query blocks have BLK rows, key blocks BK keys (BK = BLK, or 32 for the
 // paper's rectangular setting with 128-row query blocks and 32-key key blocks);
-// the keys stream through LDS in tiles of BLK keys either way.
+// the keys stream through LDS in tiles of BLK keys (64 at d = 128 with
+// 128-row blocks, where a 128-key block's sums are carried across its two
+// tiles).
 //
 // The normaliser lse_q is known only after all keys are seen.  Two schemes:
 //
@@ -46,7 +48,7 @@ namespace {
 
 // Keys per LDS tile: 64 at d = 128 with 128-row query blocks (a tile of scores
 // then takes 32 registers instead of 64, and two 16 KiB tiles leave LDS for
-// three workgroups per CU), else one tile per query block's worth of keys.
+// four workgroups per CU), else one query block's worth of keys.
 constexpr int cal_tile_keys(int d, int blk) { return (d == 128 && blk == 128) ? 64 : blk; }
 
 template <int D, int BLK>
