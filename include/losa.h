@@ -60,7 +60,15 @@ typedef enum {
   LOSA_ERR_HIP = 7            /* a HIP runtime / launch error; see losa_last_error()      */
 } losa_status;
 
-typedef enum { LOSA_DTYPE_F32 = 0, LOSA_DTYPE_BF16 = 1 } losa_dtype;
+typedef enum {
+  LOSA_DTYPE_F32 = 0,
+  LOSA_DTYPE_BF16 = 1,
+  /* not element types: they give losa_dtype the range of int, so that any int
+     a caller passes is a value of the type and is rejected with
+     LOSA_ERR_UNSUPPORTED instead of being out of the enumeration's range */
+  LOSA_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+  LOSA_DTYPE_RANGE_MAX_ = 2147483647
+} losa_dtype;
 
 /*
  * Exact block attention masses of one dense step (Sec. 3.1, Eq. (1); used at
