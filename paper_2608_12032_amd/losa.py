@@ -14,7 +14,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liblosa.so")
+# the in-tree build; LOSA_LIBRARY names another build of the same sources
+# (the host-sanitizer check uses it)
+LIB_PATH = os.environ.get("LOSA_LIBRARY") or os.path.join(_HERE, "liblosa.so")
 
 LOSA_DTYPE_F32 = 0
 LOSA_DTYPE_BF16 = 1
