@@ -26,7 +26,7 @@ from oracle import losa_oracle as O
 pytestmark = pytest.mark.gpu
 
 BLOCKS = [(64, 64), (128, 128), (128, 32), (64, 32)]
-SEEDS = list(range(48))
+SEEDS = list(range(200))
 
 
 @pytest.fixture(scope="module")
