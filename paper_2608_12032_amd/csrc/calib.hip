@@ -21,8 +21,8 @@
 //      score costs one fma, one exp2 and one add;
 //   2. S^T again (identical MFMA order, so identical scores), p = exp2(x -
 //      lse2_q), summed per lane, then across the wave; each wave parks its
-//      per-tile partial in LDS and the workgroup adds the waves' partials in a
-//      fixed order at the end.  No atomics: the result is bitwise repeatable.
+//      per-key-block partial in LDS and the workgroup adds the waves' partials
+//      in a fixed order at the end.  No atomics: the result is bitwise repeatable.
 //
 // One sweep with block statistics (STATS): sweep 1 alone, and for every
 // query q and key block j it also stores
