@@ -475,10 +475,12 @@ def test_deterministic(L, key):
 # the frozen support is checked at the reuse steps of the measurement: Wan and
 # CogVideoX shapes at steps 0, 1, 25, 49; HunyuanVideo at 0, 1, 49
 FULL_STEPS = {"wan": (0, 1, 25, 49), "cog": (0, 1, 25, 49), "hunyuan": (0, 1, 49),
-              "wan-c32": (0, 1, 49), "hunyuan-c32": (0, 1), "wan-b2": (0, 1)}
+              "wan-c32": (0, 1, 49), "hunyuan-c32": (0, 1), "wan-b2": (0, 1),
+              "cog-c32": (0, 1, 49)}
 
 
-@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32", "hunyuan-c32", "wan-b2"])
+@pytest.mark.parametrize("key", ["wan", "cog", "hunyuan", "wan-c32", "hunyuan-c32", "wan-b2",
+                                 "cog-c32"])
 def test_full_size_sampled(L, key):
     # wan-b2: the Wan shape with a batch of two (the two classifier-free guidance
     # branches of a step are batch entries b = 0, 1, each with its own support)
