@@ -80,24 +80,38 @@ __device__ __forceinline__ void issue_tile(char* buf, __amdgpu_buffer_rsrc_t rs,
   }
 }
 
+// S^T of a tile's KB 32-key sub-blocks, k-step by k-step (the sub-blocks'
+// chains interleaved); each MFMA's K operand is read from LDS NPRE MFMAs ahead
+// into a small register ring, an order fixed with sched_group_barrier (left to
+// itself the compiler issued each read just before its MFMA, which then waited
+// out the LDS latency: 2 % slower at the Wan shape).
 template <int D, int BLK>
 __device__ __forceinline__ void tile_scores(const char* buf, const bf16x8_t* qreg, int l32, int g,
                                             f32x16_t* sacc) {
   using C = CalCfg<D, BLK>;
+  constexpr int NM = C::KS * C::KB;
+  constexpr int NPRE = 4;  // MFMAs an operand read leads by
   const int ksw = l32 % C::KCH;
+  auto rd = [&](int i) -> bf16x8_t {
+    const int st = i / C::KB, kb = i % C::KB;
+    const int off = (((2 * st + g) ^ ksw) << 4);
+    return *reinterpret_cast<const bf16x8_t*>(buf + (kb * 32 + l32) * C::KROW + off);
+  };
+  bf16x8_t ring[NPRE];
 #pragma unroll
-  for (int kb = 0; kb < C::KB; ++kb)
+  for (int i = 0; i < NPRE; ++i) ring[i] = rd(i);
 #pragma unroll
-    for (int t = 0; t < 16; ++t) sacc[kb][t] = 0.f;
+  for (int i = 0; i < NM; ++i) {
+    const int st = i / C::KB, kb = i % C::KB;
+    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % NPRE], qreg[st],
+                                                       st == 0 ? f32x16_t{} : sacc[kb], 0, 0, 0);
+    if (i + NPRE < NM) ring[i % NPRE] = rd(i + NPRE);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, NPRE, 0);
 #pragma unroll
-  for (int s = 0; s < C::KS; ++s) {
-    const int off = (((2 * s + g) ^ ksw) << 4);
-#pragma unroll
-    for (int kb = 0; kb < C::KB; ++kb) {
-      const bf16x8_t a =
-          *reinterpret_cast<const bf16x8_t*>(buf + (kb * 32 + l32) * C::KROW + off);
-      sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[s], sacc[kb], 0, 0, 0);
-    }
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i + NPRE < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
 }
 
